@@ -1,0 +1,47 @@
+"""The oracle's pins are sensitive: each plausible mistake planted in a copy of
+the oracle source (a dropped term, a wrong index, a flipped comparison) must
+make the pin suite fail.  Mutants are built and run on the CPU only."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PIN_FILES = ["tests/test_oracle_fuse.py", "tests/test_oracle_decode.py",
+             "tests/test_oracle_evict.py", "tests/test_oracle_offsets.py"]
+
+MUTANTS = {
+    "drop_decay": ("score_out[(size_t)l * T + j] = gamma * prev + psum[j];",
+                   "score_out[(size_t)l * T + j] = prev + psum[j];"),
+    "scale_by_d": ("sm_scale = 1.0 / sqrt((double)d);", "sm_scale = 1.0 / (double)d;"),
+    "gqa_modulo": ("(int32_t)(((int64_t)h * Hkv) / Hq)", "(int32_t)(h % Hkv)"),
+    "no_normalise": ("                s[j] /= z;\n", "\n"),
+    "new_key_from_cache": (": ld(k_new, dtype, nb + c);", ": ld(k_cache, dtype, cb + (size_t)j * d + c);"),
+    "new_slot_nonzero": ("double prev = (j < len) ? score_in[(size_t)l * cap + j] : 0.0;",
+                         "double prev = (j < len) ? score_in[(size_t)l * cap + j] : 1.0;"),
+    "mean_divisor": ("double mean = sum / (double)count;", "double mean = sum / (double)(count + 1);"),
+    "anchor_subtracted": ("mean += ld(anchor,", "mean -= ld(anchor,"),
+    "topn_ascending": ("if (x->score > y->score)", "if (x->score < y->score)"),
+    "recent_off_by_one": ("c.pos >= next_pos - M", "c.pos > next_pos - M"),
+    "sink_off_by_one": ("c.pos < n_sink", "c.pos <= n_sink"),
+    "eq3_round_up": ("((int64_t)L_a * te) / t_total_ms", "((int64_t)L_a * te + t_total_ms - 1) / t_total_ms"),
+    "groups_not_min": ("int64_t g = seg[i].lt < len ? seg[i].lt : len;", "int64_t g = len;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(os.path.join(ROOT, "oracle", "voxzip_oracle.c")).read()
+    assert src.count(old) == 1, f"mutation site for {name} is not unique"
+    mutant_src = tmp_path / "mutant.c"
+    mutant_src.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libmutant.so")
+    oracle.build(out=lib, src=str(mutant_src))
+    env = dict(os.environ, VOXZIP_ORACLE_LIB=lib, OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", *PIN_FILES],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode == 1, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
