@@ -1,0 +1,172 @@
+/*
+ * voxzip.h -- C ABI of libvoxzip.so, the MI355X (gfx950) hot path of VoxZip
+ * ("Semantic-Anchored Temporal KV Cache Compression for Long-Context Audio
+ * Inference", arXiv 2608.08569).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are DEVICE pointers unless marked [host].  The caller owns all
+ *    memory; the library allocates nothing and keeps no state between calls
+ *    (thread-safe as long as concurrent calls do not share buffers).
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ *    is the default stream).  Errors found on the host are returned before any
+ *    work is queued; a failed launch returns VZ_ERR_HIP.
+ *  - KV caches are [n_layers][kv_heads][cap][d], contiguous in d.  The element
+ *    type of q, k, v, caches and outputs is `dtype` (VZ_F32 or VZ_BF16);
+ *    scores are float32 [n_layers][cap]; positions are int32 [n_layers][cap].
+ *    All layers hold the same number of resident tokens `len`.
+ *  - Supported shapes: d in {64, 128}; n_q_heads a multiple of kv_heads with
+ *    n_q_heads / kv_heads <= 16; every size positive and every index below 2^31.
+ *  - Slots are not kept in position order: each slot carries its logical
+ *    position in `pos`, and the sink and recent windows are defined on
+ *    positions.  Positions inside one layer must be distinct.
+ */
+#ifndef VOXZIP_H
+#define VOXZIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define VZ_API __attribute__((visibility("default")))
+#else
+#define VZ_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define VZ_OK 0
+#define VZ_ERR_INVALID -1     /* a null pointer, a bad scalar (gamma, budget, windows) */
+#define VZ_ERR_SHAPE -2       /* inconsistent sizes (n_q_heads % kv_heads, d, counts) */
+#define VZ_ERR_CAPACITY -3    /* the cache or an output has no room */
+#define VZ_ERR_UNSUPPORTED -4 /* dtype / head size / group size this build does not serve */
+#define VZ_ERR_HIP -5         /* a HIP call failed; voxzip_last_error() has its text */
+#define VZ_ERR_WORKSPACE -6   /* workspace missing or smaller than voxzip_workspace_bytes() */
+
+/* Element types. */
+#define VZ_F32 0
+#define VZ_BF16 1
+
+/* Operations whose workspace can be queried. */
+#define VZ_OP_DECODE 1
+#define VZ_OP_EVICT 2
+
+/*
+ * Stage-1 semantic-anchored fusion (Sec. 3.2.1, Eq. 4 group average pooling,
+ * the additive text anchor that follows it, and the chronological
+ * concatenation of Eq. 5), applied to each layer's K and V per KV head.
+ *
+ *   k_out[l][h][j][:] = mean(k_in[l][h][span_off[j] .. span_off[j+1]-1][:])
+ *                       (+ anchor_k[l][h][j][:] when anchor_k is not NULL)
+ *   and the same for v; pos_out[l][j] = j; score_out[l][j] = 0
+ *   for every layer l, KV head h and span j < n_spans.
+ *
+ *  k_in, v_in   [n_layers][kv_heads][T_in][d]  input (prefill) K and V.
+ *  span_off     int32 [n_spans + 1], device.  Groups are contiguous and in
+ *               time order: span_off[0] = 0, strictly increasing,
+ *               span_off[n_spans] = T_in.  A background token is a span of
+ *               length 1 (and is copied bit for bit).  Offsets are not read on
+ *               the host; the kernel clamps them into [0, T_in], so malformed
+ *               offsets give unspecified rows but never an out-of-range access.
+ *  anchor_k/v   NULL, or [n_layers][kv_heads][n_spans][d] rows added after the mean.
+ *  k_out, v_out [n_layers][kv_heads][cap_out][d]; slots >= n_spans untouched.
+ *  score_out    float32 [n_layers][cap_out]; pos_out int32 [n_layers][cap_out].
+ * Arithmetic: float32 sum in row order, IEEE division by the span length,
+ * float32 anchor add, one rounding to dtype (nearest-even).
+ * Errors: VZ_ERR_INVALID for null pointers or k_in/v_in aliasing an output,
+ * VZ_ERR_CAPACITY if n_spans > cap_out, VZ_ERR_SHAPE if n_spans > T_in.
+ */
+VZ_API int voxzip_fuse_spans(const void *k_in, const void *v_in, int32_t T_in,
+                      const int32_t *span_off, int32_t n_spans,
+                      const void *anchor_k, const void *anchor_v,
+                      void *k_out, void *v_out, float *score_out, int32_t *pos_out,
+                      int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap_out,
+                      int32_t dtype, void *stream);
+
+/*
+ * One decode step for every layer: Sec. 3.1 Eq. 1 (append), Eq. 2 (attention)
+ * and Sec. 3.2.2 Eq. 6 (temporally decayed accumulated score).
+ *
+ *  1. Append: k_cache/v_cache[l][g][len] = k_new/v_new[l][g];
+ *     pos[l][len] = next_pos; the new slot's previous score is 0.
+ *  2. Attend over slots 0..len (T = len + 1 keys): query head h reads KV head
+ *     g = h / (n_q_heads / kv_heads);
+ *       p[l][h][j] = softmax_j(sm_scale * q[l][h] . K[l][g][j]),
+ *       out[l][h]  = sum_j p[l][h][j] * V[l][g][j].
+ *  3. Score: score[l][j] = gamma * score[l][j] + sum_h p[l][h][j]  (j <= len).
+ *
+ *  q, out       [n_layers][n_q_heads][d];  k_new, v_new [n_layers][kv_heads][d].
+ *  k_cache, v_cache, score, pos   in/out; slot len must exist (len + 1 <= cap).
+ *  gamma        decay in [0, 1] (1 = plain accumulation).
+ *  sm_scale     softmax scale; <= 0 selects 1 / sqrt(d).
+ *  workspace    device scratch of at least voxzip_workspace_bytes(VZ_OP_DECODE,
+ *               ...) bytes.  It must be zero-filled once after allocation; the
+ *               kernels leave it zeroed again when they finish.  One workspace
+ *               must not be used by two calls that can run at the same time.
+ * The caller advances len and next_pos by one after the call.
+ * Errors: VZ_ERR_INVALID (null pointer, gamma outside [0,1], len < 0),
+ * VZ_ERR_CAPACITY (len + 1 > cap), VZ_ERR_SHAPE, VZ_ERR_UNSUPPORTED,
+ * VZ_ERR_WORKSPACE.
+ */
+VZ_API int voxzip_decode_attend_score(const void *q, const void *k_new, const void *v_new,
+                               void *k_cache, void *v_cache, float *score, int32_t *pos,
+                               void *out, int32_t len, int32_t next_pos,
+                               float gamma, float sm_scale,
+                               int32_t n_layers, int32_t n_q_heads, int32_t kv_heads,
+                               int32_t d, int32_t cap, int32_t dtype,
+                               void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Stage-2 eviction with in-place compaction (Sec. 3.2.2, Eq. 7-9).
+ *
+ * If len <= budget nothing moves.  Otherwise, per layer, with
+ * M = n_recent (or budget / 5 when n_recent < 0) and T = n_sink:
+ *   sinks   = slots with pos < T,
+ *   recent  = slots with pos >= next_pos - M,
+ *   middle  = the other slots;
+ *   keep the N = budget - |sinks| - |recent| middle slots with the largest
+ *   score (equal scores: the smaller position is kept), together with every
+ *   sink and recent slot.  The kept rows of K, V, score and pos end up in slots
+ *   0 .. budget-1 (kept rows already below `budget` do not move; kept rows above
+ *   it fill the freed slots), so the resident set equals the concatenation of
+ *   Eq. 7-8 up to slot order.
+ *  next_pos     one past the newest position (positions must be < next_pos).
+ *  kept_pos_out NULL, or int32 [n_layers][budget]: kept positions, ascending
+ *               (filled also when nothing is evicted; needs next_pos <= 2^18).
+ *  new_len_out  [host] receives min(len, budget).
+ *  workspace    at least voxzip_workspace_bytes(VZ_OP_EVICT, ...) bytes.
+ * Scores must be finite; -0 ranks as +0.
+ * Errors: VZ_ERR_INVALID (null pointer, budget < 1, n_sink < 0,
+ * n_sink + M > budget), VZ_ERR_CAPACITY (len > cap), VZ_ERR_SHAPE,
+ * VZ_ERR_UNSUPPORTED, VZ_ERR_WORKSPACE.
+ */
+VZ_API int voxzip_evict_compact(void *k_cache, void *v_cache, float *score, int32_t *pos,
+                         int32_t len, int32_t budget, int32_t n_sink, int32_t n_recent,
+                         int32_t next_pos, int32_t *kept_pos_out, int32_t *new_len_out,
+                         int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap,
+                         int32_t dtype, void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Workspace bytes an operation needs for the given sizes (0 on a bad op).
+ * n_q_heads is ignored for VZ_OP_EVICT.
+ */
+VZ_API size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_heads,
+                              int32_t kv_heads, int32_t d, int32_t cap);
+
+/* Text of a status code (static storage). */
+VZ_API const char *voxzip_status_string(int status);
+
+/* Text of the last error raised on the calling thread ("" if none). */
+VZ_API const char *voxzip_last_error(void);
+
+/* ABI version, major * 100 + minor. */
+VZ_API int voxzip_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VOXZIP_H */

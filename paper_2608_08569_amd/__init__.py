@@ -1,0 +1,137 @@
+"""VoxZip hot path on MI355X: Python binding of libvoxzip.so.
+
+The functions below carry the names of the C entry points in
+``include/voxzip.h`` and only marshal arguments: torch tensors are passed as
+device pointers together with their sizes and the current HIP stream.  All
+work runs in the library's HIP kernels.  There is no fallback: if the library
+is not built, importing the binding's functions raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("VOXZIP_LIB", os.path.join(HERE, "libvoxzip.so"))
+
+VZ_OK, VZ_ERR_INVALID, VZ_ERR_SHAPE, VZ_ERR_CAPACITY = 0, -1, -2, -3
+VZ_ERR_UNSUPPORTED, VZ_ERR_HIP, VZ_ERR_WORKSPACE = -4, -5, -6
+VZ_F32, VZ_BF16 = 0, 1
+VZ_OP_DECODE, VZ_OP_EVICT = 1, 2
+
+_lib = None
+
+
+class VoxzipError(RuntimeError):
+    def __init__(self, status: int, text: str):
+        super().__init__(f"{text} (status {status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C library with argument types declared."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                          "or python paper_2608_08569_amd/build.py")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    L.voxzip_fuse_spans.argtypes = [P, P, i32, P, i32, P, P, P, P, P, P, i32, i32, i32, i32, i32, P]
+    L.voxzip_decode_attend_score.argtypes = [P, P, P, P, P, P, P, P, i32, i32, f32, f32,
+                                             i32, i32, i32, i32, i32, i32, P, sz, P]
+    L.voxzip_evict_compact.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, P, P,
+                                       i32, i32, i32, i32, i32, P, sz, P]
+    L.voxzip_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+    L.voxzip_workspace_bytes.restype = sz
+    for f in (L.voxzip_fuse_spans, L.voxzip_decode_attend_score, L.voxzip_evict_compact):
+        f.restype = ctypes.c_int
+    L.voxzip_status_string.argtypes = [ctypes.c_int]
+    L.voxzip_status_string.restype = ctypes.c_char_p
+    L.voxzip_last_error.restype = ctypes.c_char_p
+    L.voxzip_version.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != VZ_OK:
+        L = lib()
+        raise VoxzipError(status, f"{L.voxzip_status_string(status).decode()}: "
+                                  f"{L.voxzip_last_error().decode()}")
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return VZ_F32
+    if t.dtype == torch.bfloat16:
+        return VZ_BF16
+    raise TypeError(f"unsupported tensor dtype {t.dtype}")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def voxzip_workspace_bytes(op: int, n_layers: int, n_q_heads: int, kv_heads: int, d: int, cap: int) -> int:
+    return int(lib().voxzip_workspace_bytes(op, n_layers, n_q_heads, kv_heads, d, cap))
+
+
+def voxzip_fuse_spans(k_in, v_in, span_off, k_out, v_out, score_out, pos_out,
+                      anchor_k=None, anchor_v=None, stream=None) -> None:
+    """Stage-1 fusion; k_in/v_in [L][H][T_in][d], k_out/v_out [L][H][cap][d],
+    span_off int32 [n+1] on the device."""
+    L, H, T_in, d = k_in.shape
+    cap = k_out.shape[2]
+    n = span_off.numel() - 1
+    _check(lib().voxzip_fuse_spans(_ptr(k_in), _ptr(v_in), T_in, _ptr(span_off), n,
+                                   _ptr(anchor_k), _ptr(anchor_v), _ptr(k_out), _ptr(v_out),
+                                   _ptr(score_out), _ptr(pos_out), L, H, d, cap,
+                                   _dtype_code(k_in), _stream(stream)))
+
+
+def voxzip_decode_attend_score(q, k_new, v_new, k_cache, v_cache, score, pos, out, length, next_pos,
+                               gamma, sm_scale=0.0, workspace=None, stream=None) -> None:
+    """One decode step over all layers; q/out [L][Hq][d], caches [L][Hkv][cap][d]."""
+    L, Hkv, cap, d = k_cache.shape
+    Hq = q.shape[1]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().voxzip_decode_attend_score(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+                                            _ptr(v_cache), _ptr(score), _ptr(pos), _ptr(out),
+                                            int(length), int(next_pos), float(gamma), float(sm_scale),
+                                            L, Hq, Hkv, d, cap, _dtype_code(k_cache), _ptr(workspace),
+                                            ws_bytes, _stream(stream)))
+
+
+def voxzip_evict_compact(k_cache, v_cache, score, pos, length, budget, next_pos, n_sink=4, n_recent=-1,
+                         kept_pos_out=None, workspace=None, stream=None) -> int:
+    """Stage-2 eviction in place; returns the new resident length."""
+    L, Hkv, cap, d = k_cache.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    new_len = ctypes.c_int32(0)
+    _check(lib().voxzip_evict_compact(_ptr(k_cache), _ptr(v_cache), _ptr(score), _ptr(pos), int(length),
+                                      int(budget), int(n_sink), int(n_recent), int(next_pos),
+                                      _ptr(kept_pos_out), ctypes.byref(new_len), L, Hkv, d, cap,
+                                      _dtype_code(k_cache), _ptr(workspace), ws_bytes, _stream(stream)))
+    return int(new_len.value)
+
+
+def workspace(op: int, n_layers: int, n_q_heads: int, kv_heads: int, d: int, cap: int, device="cuda"):
+    """A zero-filled workspace tensor of the size the library asks for."""
+    import torch
+    n = voxzip_workspace_bytes(op, n_layers, n_q_heads, kv_heads, d, cap)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)

@@ -1,0 +1,167 @@
+// Host side of libvoxzip: argument validation, workspace sizing, status
+// strings and dispatch to the kernel launchers.  Every check runs on the host
+// before any HIP call, so invalid arguments never reach the GPU.
+#include <math.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "vz_internal.h"
+
+size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
+hipError_t vz_launch_decode_generic(const VzDecodeArgs& a, hipStream_t stream);
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fn, const char* what) {
+    g_last_error = std::string(fn) + ": " + what;
+    return status;
+}
+
+int hip_fail(const char* fn, hipError_t e) {
+    g_last_error = std::string(fn) + ": " + hipGetErrorString(e);
+    return VZ_ERR_HIP;
+}
+
+size_t elem_size(int32_t dtype) { return dtype == VZ_F32 ? 4 : 2; }
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const char* pa = static_cast<const char*>(a);
+    const char* pb = static_cast<const char*>(b);
+    return pa < pb + nb && pb < pa + na;
+}
+
+int check_common(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtype) {
+    if (L < 1 || Hkv < 1 || d < 1) return fail(VZ_ERR_SHAPE, fn, "sizes must be positive");
+    if (dtype != VZ_F32 && dtype != VZ_BF16) return fail(VZ_ERR_UNSUPPORTED, fn, "dtype must be VZ_F32 or VZ_BF16");
+    if (d != 64 && d != 128) return fail(VZ_ERR_UNSUPPORTED, fn, "head size must be 64 or 128");
+    return VZ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int voxzip_version(void) { return 100; }
+
+const char* voxzip_last_error(void) { return g_last_error.c_str(); }
+
+const char* voxzip_status_string(int status) {
+    switch (status) {
+        case VZ_OK: return "ok";
+        case VZ_ERR_INVALID: return "invalid argument";
+        case VZ_ERR_SHAPE: return "inconsistent shape";
+        case VZ_ERR_CAPACITY: return "capacity exceeded";
+        case VZ_ERR_UNSUPPORTED: return "unsupported configuration";
+        case VZ_ERR_HIP: return "HIP error";
+        case VZ_ERR_WORKSPACE: return "workspace too small";
+        default: return "unknown status";
+    }
+}
+
+size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
+                              int32_t cap) {
+    if (n_layers < 1 || kv_heads < 1 || d < 1 || cap < 1) return 0;
+    if (op == VZ_OP_DECODE) {
+        if (n_q_heads < 1) return 0;
+        return vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap);
+    }
+    if (op == VZ_OP_EVICT) return vz_evict_ws_bytes(n_layers, kv_heads, d, cap);
+    return 0;
+}
+
+int voxzip_fuse_spans(const void* k_in, const void* v_in, int32_t T_in, const int32_t* span_off, int32_t n_spans,
+                      const void* anchor_k, const void* anchor_v, void* k_out, void* v_out, float* score_out,
+                      int32_t* pos_out, int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap_out,
+                      int32_t dtype, void* stream) {
+    static const char* fn = "voxzip_fuse_spans";
+    if (!k_in || !v_in || !span_off || !k_out || !v_out || !score_out || !pos_out)
+        return fail(VZ_ERR_INVALID, fn, "null pointer");
+    if ((anchor_k == nullptr) != (anchor_v == nullptr))
+        return fail(VZ_ERR_INVALID, fn, "anchor_k and anchor_v must both be given or both be NULL");
+    int rc = check_common(fn, n_layers, kv_heads, d, dtype);
+    if (rc) return rc;
+    if (T_in < 0 || n_spans < 0 || cap_out < 1) return fail(VZ_ERR_SHAPE, fn, "negative size");
+    if (n_spans > T_in) return fail(VZ_ERR_SHAPE, fn, "more spans than input tokens");
+    if (n_spans > cap_out) return fail(VZ_ERR_CAPACITY, fn, "n_spans exceeds cap_out");
+    const size_t es = elem_size(dtype);
+    const size_t in_bytes = static_cast<size_t>(n_layers) * kv_heads * T_in * d * es;
+    const size_t out_bytes = static_cast<size_t>(n_layers) * kv_heads * cap_out * d * es;
+    const void* ins[2] = {k_in, v_in};
+    void* outs[2] = {k_out, v_out};
+    for (const void* i : ins)
+        for (void* o : outs)
+            if (in_bytes && overlaps(i, in_bytes, o, out_bytes))
+                return fail(VZ_ERR_INVALID, fn, "an input aliases an output");
+    if (overlaps(k_out, out_bytes, v_out, out_bytes)) return fail(VZ_ERR_INVALID, fn, "k_out and v_out overlap");
+    hipError_t e = vz_launch_fuse(k_in, v_in, T_in, span_off, n_spans, anchor_k, anchor_v, k_out, v_out, score_out,
+                                  pos_out, n_layers, kv_heads, d, cap_out, dtype, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+int voxzip_decode_attend_score(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                               float* score, int32_t* pos, void* out, int32_t len, int32_t next_pos, float gamma,
+                               float sm_scale, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
+                               int32_t cap, int32_t dtype, void* workspace, size_t ws_bytes, void* stream) {
+    static const char* fn = "voxzip_decode_attend_score";
+    if (!q || !k_new || !v_new || !k_cache || !v_cache || !score || !pos || !out)
+        return fail(VZ_ERR_INVALID, fn, "null pointer");
+    int rc = check_common(fn, n_layers, kv_heads, d, dtype);
+    if (rc) return rc;
+    if (n_q_heads < 1 || n_q_heads % kv_heads != 0)
+        return fail(VZ_ERR_SHAPE, fn, "n_q_heads must be a positive multiple of kv_heads");
+    if (n_q_heads / kv_heads > 16) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 16 query heads per KV head");
+    if (n_q_heads > 256) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 256 query heads");
+    if (len < 0 || next_pos < 0) return fail(VZ_ERR_INVALID, fn, "negative len or next_pos");
+    if (cap < 1 || len + 1 > cap) return fail(VZ_ERR_CAPACITY, fn, "no free slot for the new token");
+    if (!(gamma >= 0.f && gamma <= 1.f)) return fail(VZ_ERR_INVALID, fn, "gamma must be in [0, 1]");
+    if (!isfinite(sm_scale)) return fail(VZ_ERR_INVALID, fn, "sm_scale must be finite");
+    const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap);
+    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    VzDecodeArgs a{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
+                   n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, ws_bytes};
+    hipError_t e = vz_launch_decode(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* pos, int32_t len, int32_t budget,
+                         int32_t n_sink, int32_t n_recent, int32_t next_pos, int32_t* kept_pos_out,
+                         int32_t* new_len_out, int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap,
+                         int32_t dtype, void* workspace, size_t ws_bytes, void* stream) {
+    static const char* fn = "voxzip_evict_compact";
+    if (!k_cache || !v_cache || !score || !pos || !new_len_out) return fail(VZ_ERR_INVALID, fn, "null pointer");
+    int rc = check_common(fn, n_layers, kv_heads, d, dtype);
+    if (rc) return rc;
+    if (len < 0 || cap < 1) return fail(VZ_ERR_INVALID, fn, "negative len or empty cache");
+    if (len > cap) return fail(VZ_ERR_CAPACITY, fn, "len exceeds cap");
+    if (budget < 1 || n_sink < 0) return fail(VZ_ERR_INVALID, fn, "budget must be >= 1 and n_sink >= 0");
+    const int32_t M = n_recent < 0 ? budget / 5 : n_recent;
+    if (static_cast<int64_t>(n_sink) + M > budget)
+        return fail(VZ_ERR_INVALID, fn, "sink and recent windows exceed the budget");
+    if (next_pos < len) return fail(VZ_ERR_INVALID, fn, "next_pos below len: positions cannot be distinct");
+    if (kept_pos_out && next_pos > (1 << 18))
+        return fail(VZ_ERR_UNSUPPORTED, fn, "kept_pos_out needs next_pos <= 262144");
+    const bool work = len > budget || kept_pos_out != nullptr;
+    if (work) {
+        const size_t need = vz_evict_ws_bytes(n_layers, kv_heads, d, cap);
+        if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    }
+    *new_len_out = len < budget ? len : budget;
+    if (!work) return VZ_OK;
+    VzEvictArgs a{k_cache, v_cache, score, pos, len, budget, n_sink, M, next_pos, kept_pos_out,
+                  n_layers, kv_heads, d, cap, dtype, workspace, ws_bytes};
+    hipError_t e = vz_launch_evict(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+}  // extern "C"
+
+size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap) {
+    (void)Hkv;
+    (void)d;
+    return vz_decode_generic_ws_bytes(L, Hq, cap);
+}
+
+hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream) { return vz_launch_decode_generic(a, stream); }

@@ -1,0 +1,160 @@
+"""GPU parity of the decode step (voxzip_decode_attend_score) and of the whole
+path with eviction, state-synced against the fp64 oracle: before every step
+the oracle starts from the GPU's own state, and every eviction selects on the
+oracle's scores rounded to float32 (so a near tie cannot flip the kept set)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from vzt import RTOL, GpuCache, check_close, from_dev, to_dev, widen
+
+pytestmark = pytest.mark.gpu
+
+
+def synced_step(g, q, kn, vn, gamma, layers=None):
+    """One GPU step checked against the oracle on ``layers`` (all by default)."""
+    t = __import__("torch")
+    K, V, S, P = g.snapshot()
+    ls = slice(None) if layers is None else layers
+    n0 = g.len
+    ref_o, ref_s, ref_p, _ = oracle.decode_step(q[ls], kn[ls], vn[ls], K[ls], V[ls], S[ls].astype(np.float64),
+                                                P[ls], n0, g.next_pos, gamma, g.dtype)
+    g.step(to_dev(q), to_dev(kn), to_dev(vn), gamma)
+    K2, V2, S2, P2 = g.snapshot()
+    o = from_dev(g.out)
+    rt = RTOL[g.dtype]
+    check_close(widen(o[ls], g.dtype), ref_o, rt, "attention output")
+    check_close(S2[ls][:, : n0 + 1], ref_s, rt, "decayed score")
+    assert np.array_equal(P2[ls][:, : n0 + 1], ref_p)
+    assert np.array_equal(K2[:, :, n0], kn) and np.array_equal(V2[:, :, n0], vn)   # Eq. 1 append
+    assert np.array_equal(K2[:, :, :n0], K[:, :, :n0]) and np.array_equal(V2[:, :, :n0], V[:, :, :n0])
+    return ref_s, (K2, V2, S2, P2)
+
+
+def synced_evict(g, ref_s, state, budget, layers=None):
+    """Evict on the oracle's float32 scores; kept set bit-exact, rows position-keyed."""
+    t = __import__("torch")
+    K2, V2, S2, P2 = state
+    ls = slice(None) if layers is None else layers
+    T = g.len
+    sc32 = S2.copy()
+    sc32[ls, :T] = ref_s.astype(np.float32)
+    g.score.copy_(t.from_numpy(sc32))
+    keep, nl = oracle.evict_select(sc32[ls].astype(np.float64), P2[ls], T, budget, 4, -1, g.next_pos)
+    kept = t.full((g.L, budget), -1, dtype=t.int32, device="cuda")
+    new_len = g.evict(budget, kept=kept)
+    assert new_len == nl == min(T, budget)
+    K3, V3, S3, P3 = g.snapshot()
+    kept = from_dev(kept)[ls]
+    Pl = P2[ls]
+    for i in range(keep.shape[0]):
+        ref_pos = Pl[i][keep[i]]
+        assert np.array_equal(kept[i, :nl], ref_pos), "kept position set"
+        order = np.argsort(P3[ls][i, :nl], kind="stable")
+        assert np.array_equal(P3[ls][i, :nl][order], ref_pos)
+        assert np.array_equal(K3[ls][i][:, :nl][:, order], K2[ls][i][:, keep[i]])
+        assert np.array_equal(V3[ls][i][:, :nl][:, order], V2[ls][i][:, keep[i]])
+        assert np.array_equal(S3[ls][i, :nl][order], sc32[ls][i, keep[i]])
+
+
+def _run_workload(w, g, steps, start_step=0, layers=None, budget=None, interval=1):
+    budget = w.budget if budget is None else budget
+    bias = synth.q_bias(w) if w.q_bias else None
+    for t in range(start_step, start_step + steps):
+        q, kn, vn = synth.decode_inputs(w, t, bias=bias)
+        ref_s, state = synced_step(g, q, kn, vn, w.gamma, layers)
+        if (t + 1) % interval == 0 and g.len > budget:
+            synced_evict(g, ref_s, state, budget, layers)
+
+
+def test_tiny_fused_no_eviction_needed():
+    """Tiny fp32 case: 64 fused spans + 32 steps stay within B = 128 (no eviction)."""
+    w = synth.workload("tiny")
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    g = GpuCache(w.n_layers, w.n_q_heads, w.kv_heads, w.d, 200, w.dtype)
+    g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
+    _run_workload(w, g, w.steps)
+    assert g.len == 64 + 32
+
+
+def test_tiny_unfused_evicts_every_step():
+    """Stage 2 alone on 512 unfused tokens with B = 128 (M = 25, N = 99): evicts from step one."""
+    w = synth.workload("tiny")
+    off = np.arange(513, dtype=np.int32)
+    g = GpuCache(w.n_layers, w.n_q_heads, w.kv_heads, w.d, 520, w.dtype)
+    g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
+    _run_workload(w, g, w.steps)
+    assert g.len == 128
+
+
+def test_layer_bf16_real_head_shape():
+    """One layer, 32Q/4KV, d = 128, bf16: ~1280 fused tokens, B = 1024, 128 steps."""
+    w = synth.workload("layer")
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n = len(off) - 1
+    g = GpuCache(w.n_layers, w.n_q_heads, w.kv_heads, w.d, n + w.steps + 1, w.dtype)
+    g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
+    _run_workload(w, g, w.steps)
+    assert g.len == w.budget
+
+
+@pytest.mark.parametrize("dtype,d,Hq,Hkv", [(synth.DT_BF16, 128, 64, 4), (synth.DT_BF16, 64, 6, 2),
+                                            (synth.DT_F32, 128, 8, 8), (synth.DT_F32, 64, 16, 1),
+                                            (synth.DT_BF16, 128, 32, 4)])
+@pytest.mark.parametrize("length", [0, 1, 255, 256, 257, 1000])
+def test_shapes_and_ragged_lengths(dtype, d, Hq, Hkv, length):
+    L, cap = 2, length + 3
+    key = synth.stream_key(21, dtype, d, Hq, Hkv, length)
+    k, v, s, p = synth.random_state(21, L, Hkv, d, cap, length, dtype, next_pos=length + 9)
+    g = GpuCache(L, Hq, Hkv, d, cap, dtype)
+    g.load(k, v, s, p, length, length + 9)
+    for t in range(2):
+        mk = lambda tag, shape: synth.as_storage(
+            synth.normal_f32(synth.stream_key(key, tag, t), int(np.prod(shape))).reshape(shape) * np.float32(1.7),
+            dtype)
+        synced_step(g, mk("q", (L, Hq, d)), mk("k", (L, Hkv, d)), mk("v", (L, Hkv, d)), 0.95)
+
+
+def test_gamma_edges_and_explicit_scale():
+    dtype, L, Hq, Hkv, d, length = synth.DT_BF16, 1, 32, 4, 128, 700
+    k, v, s, p = synth.random_state(3, L, Hkv, d, length + 2, length, dtype)
+    for gamma in (0.0, 1.0):
+        g = GpuCache(L, Hq, Hkv, d, length + 2, dtype)
+        g.load(k, v, s, p, length, length)
+        q, kn, vn = (synth.as_storage(synth.normal_f32(synth.stream_key(3, x), n).reshape(sh), dtype)
+                     for x, n, sh in (("q", L * Hq * d, (L, Hq, d)), ("k", L * Hkv * d, (L, Hkv, d)),
+                                      ("v", L * Hkv * d, (L, Hkv, d))))
+        synced_step(g, q, kn, vn, gamma)
+        # total mass: gamma * previous + Hq
+        S = from_dev(g.score)[0, : length + 1].astype(np.float64)
+        expect = gamma * s[0, :length].astype(np.float64).sum() + Hq
+        assert abs(S.sum() - expect) <= 1e-4 * expect
+
+
+def test_deterministic_bits():
+    """Two identical steps from the same state give identical bits."""
+    w = synth.workload("layer")
+    k, v, s, p = synth.random_state(8, 1, 4, 128, 2100, 2048, synth.DT_BF16, next_pos=3000)
+    q, kn, vn = synth.decode_inputs(w, 0)
+    outs = []
+    for _ in range(2):
+        g = GpuCache(1, 32, 4, 128, 2100, synth.DT_BF16)
+        g.load(k, v, s, p, 2048, 3000)
+        g.step(to_dev(q), to_dev(kn), to_dev(vn), 0.95)
+        outs.append((from_dev(g.out), *g.snapshot()))
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
+
+
+def test_long32k_full_size_sampled_layers():
+    """The 48-layer 32k-token workload at full size: fuse, then decode steps with
+    eviction; layers 0 and 47 are checked against the oracle every step."""
+    w = synth.workload("long32k")
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n = len(off) - 1
+    cap = max(n, w.budget) + 32
+    g = GpuCache(w.n_layers, w.n_q_heads, w.kv_heads, w.d, cap, w.dtype)
+    g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
+    _run_workload(w, g, 6, layers=[0, 47])
+    assert g.len == min(n + 6, w.budget) or g.len == w.budget
