@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Benchmark of the VoxZip hot path on one MI355X.
+
+Workload: the 32k-context long-audio cache -- 48 layers, 32 query / 4 KV
+heads, head size 128, bfloat16, 32,768 audio tokens fused by Stage 1 into
+~8.2k span tokens, budget B = 8192 (4x), gamma = 0.95, 256 decode steps with
+an eviction check after every step.
+
+One bench step = one request over that workload: Stage-1 fusion of the
+prefill cache, then 256 decode steps (append, attention, decayed score,
+eviction).  Inputs are generated once and stay resident in HBM.  The value is
+decode tokens per second over whole requests (fusion included).
+
+Also reported:
+  roofline      the decode kernel (the dominant one): algorithmic bytes per
+                launch over its mean duration, timed with HIP events on the
+                stream it runs on, against 8 TB/s;
+  cpu_baseline  the fp64 oracle on the host cores over a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+PROFILE_PMC = os.path.join(ROOT, "profiles", "decode_long32k_pmc.md")
+KERNEL_SRC = [os.path.join(ROOT, "paper_2608_08569_amd", "csrc", f)
+              for f in ("decode_fused.hip", "decode_generic.hip")]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def decode_bytes_per_layer(T, Hq, Hkv, d, s):
+    """Algorithmic HBM bytes of one decode launch, per layer: every resident
+    key and value row once, the score read-modify-write, the appended row, q and o."""
+    return T * (2 * Hkv * d * s + 8) + 2 * Hkv * d * s + 2 * Hq * d * s
+
+
+def evict_bytes_per_layer(T, E, Hkv, d, s):
+    """Score and position read of every slot plus the moved rows (read + write)."""
+    return 8 * T + 2 * E * (2 * Hkv * d * s + 8)
+
+
+def kernel_sha() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SRC:
+        if os.path.exists(p):
+            h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic():
+    """HBM bytes per decode launch from the committed rocprofv3 counter summary,
+    only if it was taken on the current kernel source."""
+    if not os.path.exists(PROFILE_PMC):
+        return None
+    txt = open(PROFILE_PMC).read()
+    m_sha = re.search(r"kernel_source_sha:\s*([0-9a-f]+)", txt)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not (m_sha and m_b) or m_sha.group(1) != kernel_sha():
+        return None
+    return float(m_b.group(1))
+
+
+def cpu_baseline(w, n_layers_sample: int, max_seconds: float):
+    """The oracle (as it stands) on a sample: the first n layers, fused on the
+    host, then decode steps with eviction until max_seconds of step time."""
+    import oracle
+    t0 = time.time()
+    lib = oracle.load()
+    ls = range(n_layers_sample)
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n = len(off) - 1
+    k_in = synth.prefill_kv(w, "k", layers=ls)
+    v_in = synth.prefill_kv(w, "v", layers=ls)
+    cap = max(n, w.budget) + 4
+    run = oracle.Run(k_in, v_in, off, w.dtype, w.n_q_heads, cap, w.gamma, w.budget, lib=lib)
+    log(f"[cpu] oracle setup {time.time() - t0:.1f}s")
+    step_times = []
+    t_all = time.time()
+    for t in range(256):
+        q, kn, vn = synth.decode_inputs(w, t)
+        ts = time.perf_counter()
+        run.step(q[:n_layers_sample], kn[:n_layers_sample], vn[:n_layers_sample])
+        step_times.append(time.perf_counter() - ts)
+        if time.time() - t_all > max_seconds:
+            break
+    per_step_all_layers = float(np.mean(step_times)) * (w.n_layers / n_layers_sample)
+    return {
+        "value": 1.0 / per_step_all_layers,
+        "unit": "tokens/s",
+        "cores": int(min(oracle.threads(lib), n_layers_sample)),
+        "kind": "oracle",
+        "sample": (f"{len(step_times)} decode steps (append, attend, score, evict) of the 32k workload on "
+                   f"{n_layers_sample} of {w.n_layers} layers, after host-side fusion; time per step "
+                   f"scaled by {w.n_layers}/{n_layers_sample} to a whole-model token"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5, help="timed requests")
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--decode-steps", type=int, default=256)
+    ap.add_argument("--cpu-layers", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the sharding design is described in the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_08569_amd as vz
+
+    vz.lib()  # fail loudly if the HIP library is not built
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+
+    if args.copy_probe:
+        n = 1 << 30
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n}))
+        return
+
+    w = synth.workload("long32k")
+    L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+    s = 2
+    t0 = time.time()
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n_spans = len(off) - 1
+    to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    k_in = to_dev(synth.prefill_kv(w, "k"))
+    v_in = to_dev(synth.prefill_kv(w, "v"))
+    off_d = torch.from_numpy(off).cuda()
+    steps_in = []
+    for t in range(args.decode_steps):
+        q, kn, vn = synth.decode_inputs(w, t)
+        steps_in.append((to_dev(q), to_dev(kn), to_dev(vn)))
+    log(f"[gpu] inputs ready in {time.time() - t0:.1f}s: {n_spans} spans")
+
+    cap = max(n_spans, w.budget) + 2
+    K = torch.zeros(L, Hkv, cap, d, dtype=torch.bfloat16, device="cuda")
+    V = torch.zeros_like(K)
+    S = torch.zeros(L, cap, dtype=torch.float32, device="cuda")
+    P = torch.zeros(L, cap, dtype=torch.int32, device="cuda")
+    out = torch.zeros(L, Hq, d, dtype=torch.bfloat16, device="cuda")
+    ws_d = vz.workspace(vz.VZ_OP_DECODE, L, Hq, Hkv, d, cap)
+    ws_e = vz.workspace(vz.VZ_OP_EVICT, L, Hq, Hkv, d, cap)
+
+    def request(timing=None):
+        """Fuse, then decode with eviction; returns (decode tokens, bytes)."""
+        ev = timing
+        if ev is not None:
+            ev["fuse"][0].record(stream)
+        vz.voxzip_fuse_spans(k_in, v_in, off_d, K, V, S, P)
+        if ev is not None:
+            ev["fuse"][1].record(stream)
+        length, nxt = n_spans, n_spans
+        total_bytes = 0
+        for t in range(args.decode_steps):
+            q, kn, vn = steps_in[t]
+            if ev is not None:
+                ev["dec"][t][0].record(stream)
+            vz.voxzip_decode_attend_score(q, kn, vn, K, V, S, P, out, length, nxt, w.gamma, workspace=ws_d)
+            if ev is not None:
+                ev["dec"][t][1].record(stream)
+            T = length + 1
+            total_bytes += L * decode_bytes_per_layer(T, Hq, Hkv, d, s)
+            length, nxt = T, nxt + 1
+            if length > w.budget:
+                E = length - w.budget
+                length = vz.voxzip_evict_compact(K, V, S, P, length, w.budget, nxt, workspace=ws_e)
+                total_bytes += L * evict_bytes_per_layer(T, E, Hkv, d, s)
+        return args.decode_steps, total_bytes
+
+    for _ in range(args.warmup):
+        request()
+    torch.cuda.synchronize()
+
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    timings = []
+    tokens = 0
+    path_bytes = 0
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        ev = {"fuse": (mk(), mk()), "dec": [(mk(), mk()) for _ in range(args.decode_steps)]}
+        tk, b = request(ev)
+        tokens += tk
+        path_bytes += b
+        timings.append(ev)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+
+    dec_ms = np.array([[a.elapsed_time(b) for a, b in ev["dec"]] for ev in timings])  # [req][step]
+    fuse_ms = np.array([ev["fuse"][0].elapsed_time(ev["fuse"][1]) for ev in timings])
+    # dominant kernel: decode over all layers at the steady-state length T = B + 1
+    T_ss = w.budget + 1
+    dec_bytes_ss = L * decode_bytes_per_layer(T_ss, Hq, Hkv, d, s)
+    steady = dec_ms[:, 16:] if dec_ms.shape[1] > 32 else dec_ms
+    dec_mean_s = float(np.mean(steady)) * 1e-3
+    achieved = dec_bytes_ss / dec_mean_s / 1e9
+    traffic = read_traffic()
+    fuse_bytes = L * Hkv * 2 * (32768 + n_spans) * d * s
+
+    result = {
+        "metric": "decode attend+score+evict tokens/s and HBM GB/s (% of peak) at 32k ctx",
+        "value": tokens / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "long32k",
+            "description": (f"48 layers, 32Q/4KV heads, d=128, bf16 KV cache; 32768 audio tokens fused to "
+                            f"{n_spans} span tokens (Stage 1), B=8192 (M=1638, N=6550, T=4), gamma=0.95; "
+                            f"one step = fusion + {args.decode_steps} decode steps with eviction"),
+            "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "audio_tokens": 32768,
+            "fused_tokens": n_spans, "budget": w.budget, "decode_steps_per_request": args.decode_steps,
+        },
+        "path_gbps": path_bytes / elapsed / 1e9,
+        "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
+        "decode_us_mean": float(np.mean(dec_ms)) * 1e3,
+        "fuse_ms_mean": float(np.mean(fuse_ms)),
+        "fuse_gbps": fuse_bytes / (float(np.mean(fuse_ms)) * 1e-3) / 1e9,
+        "roofline": {
+            "kernel": "voxzip_decode_attend_score (48 layers, T=8193)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": dec_bytes_ss,
+            "mean_launch_us": dec_mean_s * 1e6,
+        },
+    }
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

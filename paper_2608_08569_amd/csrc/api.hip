@@ -8,9 +8,6 @@
 
 #include "vz_internal.h"
 
-size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
-hipError_t vz_launch_decode_generic(const VzDecodeArgs& a, hipStream_t stream);
-
 namespace {
 
 thread_local std::string g_last_error;
@@ -161,7 +158,12 @@ int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* po
 size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap) {
     (void)Hkv;
     (void)d;
-    return vz_decode_generic_ws_bytes(L, Hq, cap);
+    const size_t gen = vz_decode_generic_ws_bytes(L, Hq, cap);
+    const size_t fused = vz_decode_fused_ws_bytes(L, Hq, cap);
+    return gen > fused ? gen : fused;
 }
 
-hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream) { return vz_launch_decode_generic(a, stream); }
+hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream) {
+    if (vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.cap)) return vz_launch_decode_fused(a, stream);
+    return vz_launch_decode_generic(a, stream);
+}

@@ -141,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(const float* __restrict_
 template <int DT, int D>
 hipError_t launch(const VzDecodeArgs& a, hipStream_t stream) {
     using T = typename vz::Elem<DT>::T;
-    float* S = static_cast<float*>(a.ws);
+    float* S = reinterpret_cast<float*>(static_cast<uint8_t*>(a.ws) + vz_decode_hdr_bytes(a.L));
     float* ml = S + static_cast<size_t>(a.L) * a.Hq * a.cap;
     const float scale = a.sm_scale > 0.f ? a.sm_scale : 1.0f / sqrtf(static_cast<float>(D));
     const int T_keys = a.len + 1;
@@ -162,7 +162,7 @@ hipError_t launch(const VzDecodeArgs& a, hipStream_t stream) {
 }  // namespace
 
 size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int32_t cap) {
-    return (static_cast<size_t>(L) * Hq * cap + static_cast<size_t>(L) * Hq * 2) * sizeof(float);
+    return vz_decode_hdr_bytes(L) + (static_cast<size_t>(L) * Hq * cap + static_cast<size_t>(L) * Hq * 2) * sizeof(float);
 }
 
 hipError_t vz_launch_decode_generic(const VzDecodeArgs& a, hipStream_t stream) {

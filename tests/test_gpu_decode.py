@@ -101,8 +101,9 @@ def test_layer_bf16_real_head_shape():
 
 @pytest.mark.parametrize("dtype,d,Hq,Hkv", [(synth.DT_BF16, 128, 64, 4), (synth.DT_BF16, 64, 6, 2),
                                             (synth.DT_F32, 128, 8, 8), (synth.DT_F32, 64, 16, 1),
-                                            (synth.DT_BF16, 128, 32, 4)])
-@pytest.mark.parametrize("length", [0, 1, 255, 256, 257, 1000])
+                                            (synth.DT_BF16, 128, 32, 4), (synth.DT_BF16, 128, 16, 1),
+                                            (synth.DT_BF16, 128, 6, 2), (synth.DT_BF16, 128, 64, 8)])
+@pytest.mark.parametrize("length", [0, 1, 15, 255, 256, 257, 1000, 5000])
 def test_shapes_and_ragged_lengths(dtype, d, Hq, Hkv, length):
     L, cap = 2, length + 3
     key = synth.stream_key(21, dtype, d, Hq, Hkv, length)
@@ -130,6 +131,17 @@ def test_gamma_edges_and_explicit_scale():
         S = from_dev(g.score)[0, : length + 1].astype(np.float64)
         expect = gamma * s[0, :length].astype(np.float64).sum() + Hq
         assert abs(S.sum() - expect) <= 1e-4 * expect
+
+
+def test_many_chunks_per_layer():
+    """65,535 resident keys: 256 chunks per layer on the fused path (its limit)."""
+    dtype, L, Hq, Hkv, d, length = synth.DT_BF16, 1, 32, 4, 128, 65535
+    k, v, s, p = synth.random_state(12, L, Hkv, d, length + 1, length, dtype)
+    g = GpuCache(L, Hq, Hkv, d, length + 1, dtype)
+    g.load(k, v, s, p, length, length)
+    w = synth.workload("layer")
+    q, kn, vn = synth.decode_inputs(w, 3)
+    synced_step(g, q, kn, vn, 0.95)
 
 
 def test_deterministic_bits():

@@ -98,11 +98,21 @@ class GpuCache:
         torch().cuda.synchronize()
         return (from_dev(self.k), from_dev(self.v), from_dev(self.score), from_dev(self.pos))
 
-    def step(self, q_dev, k_dev, v_dev, gamma, sm_scale=0.0):
+    def step(self, q_dev, k_dev, v_dev, gamma, sm_scale=0.0, check_ws=True):
         self.vz.voxzip_decode_attend_score(q_dev, k_dev, v_dev, self.k, self.v, self.score, self.pos, self.out,
                                            self.len, self.next_pos, gamma, sm_scale, workspace=self.ws_dec)
         self.len += 1
         self.next_pos += 1
+        if check_ws:
+            self.check_decode_workspace()
+
+    def check_decode_workspace(self):
+        """The decode workspace header (ticket, done, error flag, per-layer
+        arrival counters) is back to zero after every call."""
+        torch().cuda.synchronize()
+        hdr = from_dev(self.ws_dec[: 256 + 4 * self.L]).view(np.uint32)
+        assert hdr[2] == 0, "decode kernel flagged an error (expired wait or unzeroed workspace)"
+        assert not hdr.any(), f"decode workspace header not cleared: {hdr[:4]}"
 
     def evict(self, budget, n_sink=4, n_recent=-1, kept=None):
         self.len = self.vz.voxzip_evict_compact(self.k, self.v, self.score, self.pos, self.len, budget,
