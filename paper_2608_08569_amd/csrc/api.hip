@@ -164,6 +164,6 @@ size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t
 }
 
 hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream) {
-    if (vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.cap)) return vz_launch_decode_fused(a, stream);
+    if (vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.cap, a.L)) return vz_launch_decode_fused(a, stream);
     return vz_launch_decode_generic(a, stream);
 }

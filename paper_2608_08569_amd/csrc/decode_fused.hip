@@ -1,10 +1,12 @@
 // Decode step (Sec. 3.1 Eq. 1-2, Sec. 3.2.2 Eq. 6) for bfloat16 caches with
-// d = 128 and at most 8 query heads per KV head: one launch for every layer,
-// attention on the matrix cores, and the decayed-score fold done from
-// registers.
+// d = 128 and at most 8 query heads per KV head.  Two launches cover every
+// layer: the attend kernel (attention on the matrix cores and the
+// decayed-score fold from registers) and a small combine kernel (the output
+// rows from the per-chunk partials).
 //
-// Work item = (layer, key chunk of <= 256 keys).  A workgroup has one wave per
-// KV head; wave g streams K and V rows of head g over the chunk:
+// Attend kernel: work item = (layer, key chunk of <= 256 keys).  A workgroup
+// has one wave per KV head; wave g streams K and V rows of head g over the
+// chunk:
 //   pass 1  S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (M = 16 keys, N = 16
 //           query-head columns of which n_q/n_kv <= 8 are used, K = 32
 //           channels).  K tiles of 32 rows are loaded fully coalesced (4 whole
@@ -15,28 +17,30 @@
 //           moved into the unused head columns 8..15 of the even tile's
 //           registers (DPP row rotate by 8), so 256 keys x 8 heads take 32
 //           registers per lane.
-//   softmax chunk-local max and sum per head; the registers then hold
-//           p~ = exp(s - m_chunk).
+//   stats   chunk-local max and sum per head; the registers then hold
+//           p~ = exp(s - m_chunk).  The (max, sum) pairs are published to the
+//           workspace at once and the chunk arrives on its layer's counter.
 //   pass 2  O += P V: V tiles of 32 keys take the same coalesced path into
 //           LDS (another swizzle) and are read back with ds_read_b64_tr_b16
 //           directly in the B-operand layout; P is rebuilt from the packed p~
-//           registers with one row rotate.
-//   The chunk writes its partial (max, sum, O) to the workspace and arrives
-//   on a per-layer counter.  Once all chunks of its layer have arrived, every
-//   chunk reads the layer's global (max, sum) per head and folds
-//       A[j] = gamma * A[j] + sum_h exp(s_hj - m_h) / l_h
-//   for its own keys from the p~ still in registers -- no logit ever goes to
-//   HBM.  Chunks then combine the partial outputs of the heads assigned to
-//   them.  Work items are taken in ticket order (one atomic per workgroup), so
-//   the chunks of a layer start together whatever order the hardware
-//   dispatches workgroups in; a layer can only wait on chunks that already
-//   hold a ticket, and the number of chunks per layer is kept below the number
-//   of workgroups that can be resident, so every wait ends.  The wait is also
-//   bounded in time: on expiry the kernel flags an error in the workspace and
-//   finishes.  The last workgroup to finish clears the counters.
-//   Cross-workgroup data (partials, counters) moves through device-scope
-//   atomic loads and stores, which are coherent across the per-XCD L2 caches,
-//   so no cache-wide flush is needed.
+//           registers with one row rotate.  The partial O goes to the
+//           workspace for the combine kernel.
+//   fold    by now the other chunks of the layer have normally published
+//           their statistics too (the wait is for their pass 1 only); the
+//           chunk reads the layer's global (max, sum) per head and folds
+//               A[j] = gamma * A[j] + sum_h exp(s_hj - m_h) / l_h
+//           for its own keys from the p~ still in registers -- no logit ever
+//           goes to HBM.
+// Work items are taken in ticket order (one atomic per workgroup), so the
+// chunks of a layer start together whatever order the hardware dispatches
+// workgroups in.  A chunk waits only for chunks of its layer that already
+// hold a ticket and never wait themselves before publishing, and the number
+// of chunks per layer is kept below the number of workgroups that can be
+// resident, so every wait ends; it is also bounded in time (on expiry the
+// kernel flags an error in the workspace and finishes).  The last workgroup
+// to finish clears the counters.  Statistics move through device-scope atomic
+// stores and loads, coherent across the per-XCD L2 caches, so no cache-wide
+// flush is needed.
 #include <math.h>
 
 #include "vz_internal.h"
@@ -55,7 +59,6 @@ constexpr int CHUNK = 16 * TILES;      // keys per chunk (at most)
 constexpr int VT = 32;                 // keys per staged tile
 constexpr int KSTEPS = D / 32;         // MFMA k-steps over the channels
 constexpr int DTILES = D / 16;         // output column tiles
-constexpr int TT_MAX = 512;            // largest workgroup (8 KV heads)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr uint64_t kWaitTicks = 20000000ull;  // 0.2 s of the 100 MHz constant clock
 constexpr int kRor8 = 0x128;           // DPP row_ror:8 (swap the halves of each 16-lane row)
@@ -81,10 +84,6 @@ __device__ __forceinline__ float ror8(float v) {
 // Device-scope (all XCDs) coherent float store / loads.
 __device__ __forceinline__ void st_dev(float* p, float v) {
     __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_dev(const float* p) {
-    return __uint_as_float(
-        __hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
 }
 __device__ __forceinline__ float2 ld_dev2(const float2* p) {
     const uint64_t v =
@@ -115,34 +114,34 @@ __device__ __forceinline__ int kswz(int r) { return r & 15; }
 __device__ __forceinline__ int vswz(int a, int b) { return ((a << 1) + ((b & 1) << 3)) & 15; }
 
 template <int NW>
-__global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
+__global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
     uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache, float* __restrict__ score,
-    int32_t* __restrict__ pos, uint16_t* __restrict__ out, int32_t len, int32_t next_pos, float gamma,
-    float scale_log2, int32_t Hq, int32_t cap, int32_t n_chunks, int32_t nc_max, int32_t n_items,
-    int32_t L, uint8_t* __restrict__ ws, size_t hdr_bytes) {
+    int32_t* __restrict__ pos, int32_t len, int32_t next_pos, float gamma, float scale_log2, int32_t Hq,
+    int32_t cap, int32_t n_chunks, int32_t nc_max, int32_t n_items, int32_t L, uint8_t* __restrict__ ws,
+    int32_t hdr_bytes) {
     __shared__ uint32_t s_item;
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][VT * D * 2];
     __shared__ float s_psum[NW][CHUNK];
-    __shared__ float2 s_mlh[GMAX * NW];
-    __shared__ float s_w[256];
-    __shared__ float s_red[TT_MAX / D][D];
 
     const int tid = threadIdx.x;
-    const int w = tid >> 6, lane = tid & 63;
+    // wave-uniform values go through readfirstlane so that addresses built
+    // from them stay scalar (buffer descriptors in SGPRs)
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int q4 = lane >> 4, r16 = lane & 15;
     const int hi = r16 >> 3;          // 0: even tile of a pair, 1: odd tile (packed lanes)
     const int hh = r16 & 7;           // query head of the group this lane's logits belong to
     const int G = Hq / NW;
+    const int g = w;                  // KV head of this wave
 
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint32_t* arrive = reinterpret_cast<uint32_t*>(ws + sizeof(WsHeader));
     float2* part_ml = reinterpret_cast<float2*>(ws + hdr_bytes);
-    float* part_o = reinterpret_cast<float*>(ws + hdr_bytes + sizeof(float2) * static_cast<size_t>(L) * nc_max * Hq);
+    float* part_o = reinterpret_cast<float*>(ws + hdr_bytes) + 2 * L * nc_max * Hq;
 
     if (tid == 0) s_item = atomicAdd(&hdr->ticket, 1u);
     __syncthreads();
-    const int item = static_cast<int>(s_item);
+    const int item = __builtin_amdgcn_readfirstlane(static_cast<int>(s_item));
     if (item >= n_items) {  // the workspace was not zero-filled: flag it, touch nothing else
         if (tid == 0) __hip_atomic_store(&hdr->error, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
@@ -152,7 +151,6 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     const int k_begin = static_cast<int>(static_cast<int64_t>(c) * T / n_chunks);
     const int k_end = static_cast<int>(static_cast<int64_t>(c + 1) * T / n_chunks);
     const int nk = k_end - k_begin;
-    const int g = w;
     const size_t head_base = (static_cast<size_t>(l) * NW + g) * static_cast<size_t>(cap) * D;
     uint16_t* Kh = k_cache + head_base;
     uint16_t* Vh = v_cache + head_base;
@@ -160,15 +158,14 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     // Eq. (1) first: the chunk holding slot len writes the new row into the
     // cache, so every key below is read from the cache the same way.
     if (len >= k_begin && len < k_end) {
-        const uint16_t* kn = k_new + (static_cast<size_t>(l) * NW + g) * D;
-        const uint16_t* vn = v_new + (static_cast<size_t>(l) * NW + g) * D;
+        const uint16_t* kn = k_new + (l * NW + g) * D;
+        const uint16_t* vn = v_new + (l * NW + g) * D;
         if (lane < 16)
-            *reinterpret_cast<uint4*>(Kh + static_cast<size_t>(len) * D + 8 * lane) =
-                *reinterpret_cast<const uint4*>(kn + 8 * lane);
+            *reinterpret_cast<uint4*>(Kh + len * D + 8 * lane) = *reinterpret_cast<const uint4*>(kn + 8 * lane);
         else if (lane < 32)
-            *reinterpret_cast<uint4*>(Vh + static_cast<size_t>(len) * D + 8 * (lane - 16)) =
+            *reinterpret_cast<uint4*>(Vh + len * D + 8 * (lane - 16)) =
                 *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
-        if (tid == 0) pos[static_cast<size_t>(l) * cap + len] = next_pos;
+        if (tid == 0) pos[l * cap + len] = next_pos;
         __threadfence_block();
     }
     __syncthreads();
@@ -177,7 +174,7 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     uint4 qv[KSTEPS];  // B operand: Q^T, column r16 = query head (zero past G)
     {
         const int hq = r16 < G ? r16 : 0;
-        const uint16_t* qrow = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(g) * G + hq) * D + 8 * q4;
+        const uint16_t* qrow = q + (l * Hq + g * G + hq) * D + 8 * q4;
 #pragma unroll
         for (int s = 0; s < KSTEPS; ++s) {
             const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * s);
@@ -186,10 +183,10 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     }
     uint8_t* buf = s_tile[w];
     // Staging: instruction m of a 32-key tile reads rows 4m..4m+3 whole
-    // (lane = row 4m + q4, 16-byte chunk r16).  Rows past the chunk end are
-    // clamped to its last row and masked out afterwards.
-    // Buffer loads: the head's rows are addressed by 32-bit offsets from a
-    // descriptor bounded to the head's cap rows (reads outside return zero).
+    // (lane = row 4m + q4, 16-byte chunk r16) with buffer loads addressed by
+    // 32-bit offsets from a descriptor bounded to the head's cap rows (reads
+    // outside it return zero).  Rows past the chunk end are clamped to its
+    // last row and masked out afterwards.
     const int region = cap * D * 2;
     const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(Kh, 0, region, kBufferDword3);
     const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(Vh, 0, region, kBufferDword3);
@@ -215,7 +212,6 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
             *reinterpret_cast<uint4*>(buf + 256 * row + 16 * (r16 ^ kswz(row))) = stg[m];
         }
         if (u + 1 < PAIRS) load_tile(krs, u + 1);
-        else load_tile(vrs, 0);
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
         f32x4 acc[2];
 #pragma unroll
@@ -238,8 +234,8 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
 
-    // chunk-local softmax statistics per head hh (8 lanes share it: q4 x hi);
-    // afterwards sp holds p~ = exp2(s - m_c)
+    // ---------------- chunk statistics, published at once ----------------
+    // per head hh (8 lanes share it: q4 x hi); afterwards sp holds p~ = exp2(s - m_c)
     float m_c = -INFINITY;
 #pragma unroll
     for (int u = 0; u < PAIRS; ++u)
@@ -259,6 +255,15 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     l_c += __shfl_xor(l_c, 16, 64);
     l_c += __shfl_xor(l_c, 32, 64);
     l_c += ror8(l_c);
+    const int pbase = (l * nc_max + c) * Hq + g * G;  // < 2^31 (checked on the host)
+    if (q4 == 0 && r16 < G) {
+        st_dev(&part_ml[pbase + r16].x, m_c);
+        st_dev(&part_ml[pbase + r16].y, l_c);
+    }
+    load_tile(vrs, 0);                   // first V tile, issued after the statistics stores
+    __builtin_amdgcn_s_waitcnt(0x0f78);  // vmcnt(8): the statistics stores have completed
+    __syncthreads();
+    if (tid == 0) __hip_atomic_fetch_add(&arrive[l], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
     // ---------------- pass 2: O = P V on the matrix cores ----------------
     f32x4 oacc[DTILES];
@@ -302,29 +307,25 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
         }
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
-
-    // ---------------- partials and the per-layer arrival ----------------
-    const size_t pbase = (static_cast<size_t>(l) * nc_max + c) * Hq + static_cast<size_t>(g) * G;
+    // partial O (read by the combine kernel after this launch): plain stores
+    {
+        float* po = part_o + pbase * D;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int h = 4 * q4 + i;  // output row = query head of the group
-        if (h < G) {
+        for (int i = 0; i < 4; ++i) {
+            const int h = 4 * q4 + i;  // output row = query head of the group
+            if (h < G) {
 #pragma unroll
-            for (int n = 0; n < DTILES; ++n) st_dev(part_o + (pbase + h) * D + 16 * n + r16, oacc[n][i]);
+                for (int n = 0; n < DTILES; ++n) po[h * D + 16 * n + r16] = oacc[n][i];
+            }
         }
     }
-    if (q4 == 0 && r16 < G) {
-        st_dev(&part_ml[pbase + r16].x, m_c);
-        st_dev(&part_ml[pbase + r16].y, l_c);
-    }
-    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's partial stores have completed
-    __syncthreads();
+
+    // ---------------- wait for the layer's statistics ----------------
     if (tid == 0) {
-        __hip_atomic_fetch_add(&arrive[l], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t t0 = wall_clock64();
         while (__hip_atomic_load(&arrive[l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
                static_cast<uint32_t>(n_chunks)) {
-            __builtin_amdgcn_s_sleep(2);
+            __builtin_amdgcn_s_sleep(1);
             if (wall_clock64() - t0 > kWaitTicks) {
                 __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 break;
@@ -333,19 +334,18 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     }
     __syncthreads();
 
-    // ---------------- global softmax statistics of this wave's heads ----------------
-    // lane (q4, r16): head hh, chunks 4 hi + q4 + 8 k; the eight lanes of a
-    // head then merge their (max, sum) pairs.
-    const size_t lbase = static_cast<size_t>(l) * nc_max * Hq;
+    // ---------------- fold: A[j] = gamma A[j] + sum_h p_hj ----------------
+    // global (max, sum) of this wave's heads: lane (q4, r16) reads head hh,
+    // chunks q4 + 4 hi + 8 k; the eight lanes of a head then merge.
     float m_h = -INFINITY, l_h = 0.f;
     {
-        const size_t hrow = lbase + static_cast<size_t>(g) * G + (hh < G ? hh : 0);
+        const float2* hrow = part_ml + l * nc_max * Hq + g * G + (hh < G ? hh : 0);
         for (int c0 = q4 + 4 * hi; c0 < n_chunks; c0 += 32) {
             float2 v[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int cc = c0 + 8 * k;
-                v[k] = ld_dev2(&part_ml[hrow + static_cast<size_t>(cc < n_chunks ? cc : c0) * Hq]);
+                v[k] = ld_dev2(hrow + (cc < n_chunks ? cc : c0) * Hq);
                 if (cc >= n_chunks) v[k] = make_float2(-INFINITY, 0.f);
             }
 #pragma unroll
@@ -355,9 +355,6 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
         merge_ml(m_h, l_h, __shfl_xor(m_h, 32, 64), __shfl_xor(l_h, 32, 64));
         merge_ml(m_h, l_h, ror8(m_h), ror8(l_h));
     }
-    if (lane < G) s_mlh[g * G + lane] = make_float2(m_h, l_h);
-
-    // ---------------- fold: A[j] = gamma A[j] + sum_h p_hj ----------------
     const float fac = (hh < G) ? exp2f(m_c - m_h) / l_h : 0.f;  // p = p~ * fac
 #pragma unroll
     for (int u = 0; u < PAIRS; ++u) {
@@ -373,41 +370,13 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
         }
     }
     __syncthreads();
+    float* lsc = score + l * cap;
     for (int k = tid; k < nk; k += 64 * NW) {
         float a = 0.f;
 #pragma unroll
         for (int gg = 0; gg < NW; ++gg) a += s_psum[gg][k];
         const int j = k_begin + k;
-        float* sc = score + static_cast<size_t>(l) * cap + j;
-        *sc = ((j < len) ? gamma * *sc : 0.f) + a;
-    }
-
-    // ---------------- outputs of the heads assigned to this chunk ----------------
-    // o_h = sum_c O_c,h exp2(m_c,h - m_h) / l_h over the layer's chunks, spread
-    // over every thread of the workgroup (channel x chunk subset).
-    constexpr int TT = 64 * NW;
-    constexpr int NSP = TT >= D ? TT / D : 1;
-    for (int h = c; h < Hq; h += n_chunks) {
-        const float mh = s_mlh[h].x, lh = s_mlh[h].y;
-        for (int cc = tid; cc < n_chunks; cc += TT)
-            s_w[cc] = exp2f(ld_dev(&part_ml[lbase + static_cast<size_t>(cc) * Hq + h].x) - mh) / lh;
-        __syncthreads();
-        const int spl = TT >= D ? tid / D : 0;
-        for (int ch = (TT >= D ? tid % D : tid); ch < D; ch += (TT >= D ? D : TT)) {
-            const float* po = part_o + (lbase + h) * D + ch;
-            float acc = 0.f;
-#pragma unroll 8
-            for (int cc = spl; cc < n_chunks; cc += NSP) acc += s_w[cc] * ld_dev(po + static_cast<size_t>(cc) * Hq * D);
-            s_red[spl][ch] = acc;
-        }
-        __syncthreads();
-        for (int ch = tid; ch < D; ch += TT) {
-            float o = 0.f;
-#pragma unroll
-            for (int k = 0; k < NSP; ++k) o += s_red[k][ch];
-            out[(static_cast<size_t>(l) * Hq + h) * D + ch] = vz::f32_to_bf16(o);
-        }
-        __syncthreads();
+        lsc[j] = ((j < len) ? gamma * lsc[j] : 0.f) + a;
     }
 
     // ---------------- the last workgroup clears the counters ----------------
@@ -421,6 +390,39 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_fused_kernel(
     }
 }
 
+// Combine kernel: one workgroup of D threads per (layer, head):
+//   o_h = sum_c O_c,h exp2(m_c,h - m_h) / l_h over the layer's chunks.
+__global__ __launch_bounds__(D) void decode_combine_kernel(const uint8_t* __restrict__ ws, uint16_t* __restrict__ out,
+                                                           int32_t Hq, int32_t n_chunks, int32_t nc_max, int32_t L,
+                                                           int32_t hdr_bytes) {
+    __shared__ float s_w[256];
+    __shared__ float s_m, s_l;
+    const int h = blockIdx.x, l = blockIdx.y, tid = threadIdx.x;
+    const float2* ml = reinterpret_cast<const float2*>(ws + hdr_bytes) + l * nc_max * Hq + h;
+    const float* po = reinterpret_cast<const float*>(ws + hdr_bytes) + 2 * L * nc_max * Hq + (l * nc_max * Hq + h) * D;
+    if (tid < 64) {  // wave 0: global (max, sum) of the head over the chunks
+        float m = -INFINITY, s = 0.f;
+        for (int cc = tid; cc < n_chunks; cc += 64) {
+            const float2 v = ml[cc * Hq];
+            merge_ml(m, s, v.x, v.y);
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) merge_ml(m, s, __shfl_xor(m, o, 64), __shfl_xor(s, o, 64));
+        if (tid == 0) {
+            s_m = m;
+            s_l = s;
+        }
+    }
+    __syncthreads();
+    const float m = s_m, inv_l = 1.0f / s_l;
+    for (int cc = tid; cc < n_chunks; cc += D) s_w[cc] = exp2f(ml[cc * Hq].x - m) * inv_l;
+    __syncthreads();
+    float acc = 0.f;
+#pragma unroll 8
+    for (int cc = 0; cc < n_chunks; ++cc) acc += s_w[cc] * po[cc * Hq * D + tid];
+    out[(l * Hq + h) * D + tid] = vz::f32_to_bf16(acc);
+}
+
 }  // namespace
 
 // ---- sizing shared with the host API ----
@@ -431,11 +433,18 @@ size_t vz_decode_hdr_bytes(int32_t L) {
 
 int32_t vz_decode_fused_chunks(int32_t T) { return (T + CHUNK - 1) / CHUNK; }
 
-bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap) {
+bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap, int32_t L) {
     if (dtype != VZ_BF16 || d != D) return false;
     if (!(Hkv == 1 || Hkv == 2 || Hkv == 4 || Hkv == 8)) return false;
     if (Hq % Hkv != 0 || Hq / Hkv > GMAX) return false;
-    return vz_decode_fused_chunks(cap) <= 256;  // chunks of one layer must fit on the GPU at once
+    // 32-bit element offsets inside the kernels: partials, scores, positions,
+    // outputs, one head's rows
+    const int64_t ncm = vz_decode_fused_chunks(cap);
+    if (static_cast<int64_t>(L) * ncm * Hq * (D + 2) >= (int64_t(1) << 31)) return false;
+    if (static_cast<int64_t>(L) * cap >= (int64_t(1) << 31)) return false;
+    if (static_cast<int64_t>(cap) * D * 2 >= (int64_t(1) << 31)) return false;
+    if (static_cast<int64_t>(L) * Hq * D >= (int64_t(1) << 31)) return false;
+    return ncm <= 256;  // chunks of one layer must fit on the GPU at once
 }
 
 size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int32_t cap) {
@@ -449,21 +458,25 @@ hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
     const int nc_max = vz_decode_fused_chunks(a.cap);
     const int n_items = a.L * n_chunks;
     const float scale = (a.sm_scale > 0.f ? a.sm_scale : 1.0f / sqrtf(static_cast<float>(D))) * kLog2e;
-    const size_t hdr = vz_decode_hdr_bytes(a.L);
+    const int hdr = static_cast<int>(vz_decode_hdr_bytes(a.L));
     auto* ws = static_cast<uint8_t*>(a.ws);
-#define VZ_LAUNCH_FUSED(NW)                                                                                      \
-    hipLaunchKernelGGL((decode_fused_kernel<NW>), dim3(n_items), dim3(64 * NW), 0, stream,                      \
+#define VZ_LAUNCH_ATTEND(NW)                                                                                     \
+    hipLaunchKernelGGL((decode_attend_kernel<NW>), dim3(n_items), dim3(64 * NW), 0, stream,                     \
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_new),                \
                        static_cast<const uint16_t*>(a.v_new), static_cast<uint16_t*>(a.k_cache),                \
-                       static_cast<uint16_t*>(a.v_cache), a.score, a.pos, static_cast<uint16_t*>(a.out), a.len, \
-                       a.next_pos, a.gamma, scale, a.Hq, a.cap, n_chunks, nc_max, n_items, a.L, ws, hdr)
+                       static_cast<uint16_t*>(a.v_cache), a.score, a.pos, a.len, a.next_pos, a.gamma, scale,    \
+                       a.Hq, a.cap, n_chunks, nc_max, n_items, a.L, ws, hdr)
     switch (a.Hkv) {
-        case 1: VZ_LAUNCH_FUSED(1); break;
-        case 2: VZ_LAUNCH_FUSED(2); break;
-        case 4: VZ_LAUNCH_FUSED(4); break;
-        case 8: VZ_LAUNCH_FUSED(8); break;
+        case 1: VZ_LAUNCH_ATTEND(1); break;
+        case 2: VZ_LAUNCH_ATTEND(2); break;
+        case 4: VZ_LAUNCH_ATTEND(4); break;
+        case 8: VZ_LAUNCH_ATTEND(8); break;
         default: return hipErrorInvalidValue;
     }
-#undef VZ_LAUNCH_FUSED
+#undef VZ_LAUNCH_ATTEND
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(decode_combine_kernel, dim3(a.Hq, a.L), dim3(D), 0, stream, ws,
+                       static_cast<uint16_t*>(a.out), a.Hq, n_chunks, nc_max, a.L, hdr);
     return hipGetLastError();
 }

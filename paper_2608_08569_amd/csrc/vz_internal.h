@@ -144,7 +144,7 @@ size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t
 // decode workspace: a header (ticket, done, error, per-layer arrival counters)
 // of vz_decode_hdr_bytes(L) bytes, then path-specific scratch
 size_t vz_decode_hdr_bytes(int32_t L);
-bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap);
+bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap, int32_t L);
 size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
 hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream);
 size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
