@@ -254,7 +254,8 @@ def main():
         "fuse_ms_mean": float(np.mean(fuse_ms)),
         "fuse_gbps": fuse_bytes / (float(np.mean(fuse_ms)) * 1e-3) / 1e9,
         "roofline": {
-            "kernel": "voxzip_decode_attend_score (48 layers, T=8193)",
+            "kernel": ("voxzip_decode_attend_score = decode_attend_kernel + decode_combine_kernel "
+                       "(48 layers, T=8193)"),
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
