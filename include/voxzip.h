@@ -103,9 +103,10 @@ VZ_API int voxzip_fuse_spans(const void *k_in, const void *v_in, int32_t T_in,
  *  gamma        decay in [0, 1] (1 = plain accumulation).
  *  sm_scale     softmax scale; <= 0 selects 1 / sqrt(d).
  *  workspace    device scratch of at least voxzip_workspace_bytes(VZ_OP_DECODE,
- *               ...) bytes.  It must be zero-filled once after allocation; the
- *               kernels leave it zeroed again when they finish.  One workspace
- *               must not be used by two calls that can run at the same time.
+ *               ...) bytes.  It must be zero-filled once after allocation;
+ *               every call leaves the parts that must start at zero zeroed
+ *               again, so later calls need no clearing.  One workspace must
+ *               not be used by two calls that can run at the same time.
  * The caller advances len and next_pos by one after the call.
  * Errors: VZ_ERR_INVALID (null pointer, gamma outside [0,1], len < 0),
  * VZ_ERR_CAPACITY (len + 1 > cap), VZ_ERR_SHAPE, VZ_ERR_UNSUPPORTED,

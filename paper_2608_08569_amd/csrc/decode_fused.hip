@@ -18,16 +18,18 @@
 //           registers (DPP row rotate by 8), so 256 keys x 8 heads take 32
 //           registers per lane.
 //   stats   chunk-local max and sum per head; the registers then hold
-//           p~ = exp(s - m_chunk).  The (max, sum) pairs are published to the
-//           workspace at once and the chunk arrives on its layer's counter.
+//           p~ = exp(s - m_chunk).  Each (max, sum) pair is published to the
+//           workspace at once with one 64-bit store; a sum is at least 1 for
+//           a non-empty chunk, so a zero sum marks a pair not yet published.
 //   pass 2  O += P V: V tiles of 32 keys take the same coalesced path into
 //           LDS (another swizzle) and are read back with ds_read_b64_tr_b16
 //           directly in the B-operand layout; P is rebuilt from the packed p~
 //           registers with one row rotate.  The partial O goes to the
 //           workspace for the combine kernel.
 //   fold    by now the other chunks of the layer have normally published
-//           their statistics too (the wait is for their pass 1 only); the
-//           chunk reads the layer's global (max, sum) per head and folds
+//           their statistics too (the wait is for their pass 1 only); each
+//           wave polls the pairs of its own heads until none is zero, merges
+//           them into the layer's (max, sum) per head and folds
 //               A[j] = gamma * A[j] + sum_h exp(s_hj - m_h) / l_h
 //           for its own keys from the p~ still in registers -- no logit ever
 //           goes to HBM.
@@ -37,10 +39,11 @@
 // hold a ticket and never wait themselves before publishing, and the number
 // of chunks per layer is kept below the number of workgroups that can be
 // resident, so every wait ends; it is also bounded in time (on expiry the
-// kernel flags an error in the workspace and finishes).  The last workgroup
-// to finish clears the counters.  Statistics move through device-scope atomic
-// stores and loads, coherent across the per-XCD L2 caches, so no cache-wide
-// flush is needed.
+// kernel flags an error in the workspace and finishes).  Statistics move
+// through device-scope atomic stores and loads, coherent across the per-XCD
+// L2 caches, so no cache-wide flush is needed.  The combine kernel, which
+// runs after every attend workgroup has finished, zeroes the pairs it has
+// read and the ticket, so the workspace is ready for the next call.
 #include <math.h>
 
 #include "vz_internal.h"
@@ -66,9 +69,8 @@ constexpr int kBufferDword3 = 0x00020000;  // raw buffer descriptor word 3 (32-b
 
 struct WsHeader {
     uint32_t ticket;
-    uint32_t done;
     uint32_t error;
-    uint32_t pad[61];
+    uint32_t pad[62];
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
@@ -81,9 +83,10 @@ __device__ __forceinline__ float ror8(float v) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kRor8, 0xF, 0xF, false));
 }
 
-// Device-scope (all XCDs) coherent float store / loads.
-__device__ __forceinline__ void st_dev(float* p, float v) {
-    __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Device-scope (all XCDs) coherent 64-bit store / load of a float pair.
+__device__ __forceinline__ void st_dev2(float2* p, float a, float b) {
+    const uint64_t v = static_cast<uint64_t>(__float_as_uint(a)) | (static_cast<uint64_t>(__float_as_uint(b)) << 32);
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float2 ld_dev2(const float2* p) {
     const uint64_t v =
@@ -135,7 +138,6 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
     const int g = w;                  // KV head of this wave
 
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
-    uint32_t* arrive = reinterpret_cast<uint32_t*>(ws + sizeof(WsHeader));
     float2* part_ml = reinterpret_cast<float2*>(ws + hdr_bytes);
     float* part_o = reinterpret_cast<float*>(ws + hdr_bytes) + 2 * L * nc_max * Hq;
 
@@ -256,14 +258,8 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
     l_c += __shfl_xor(l_c, 32, 64);
     l_c += ror8(l_c);
     const int pbase = (l * nc_max + c) * Hq + g * G;  // < 2^31 (checked on the host)
-    if (q4 == 0 && r16 < G) {
-        st_dev(&part_ml[pbase + r16].x, m_c);
-        st_dev(&part_ml[pbase + r16].y, l_c);
-    }
-    load_tile(vrs, 0);                   // first V tile, issued after the statistics stores
-    __builtin_amdgcn_s_waitcnt(0x0f78);  // vmcnt(8): the statistics stores have completed
-    __syncthreads();
-    if (tid == 0) __hip_atomic_fetch_add(&arrive[l], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (q4 == 0 && r16 < G) st_dev2(&part_ml[pbase + r16], m_c, l_c);
+    load_tile(vrs, 0);
 
     // ---------------- pass 2: O = P V on the matrix cores ----------------
     f32x4 oacc[DTILES];
@@ -320,36 +316,44 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
         }
     }
 
-    // ---------------- wait for the layer's statistics ----------------
-    if (tid == 0) {
-        const uint64_t t0 = wall_clock64();
-        while (__hip_atomic_load(&arrive[l], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-               static_cast<uint32_t>(n_chunks)) {
-            __builtin_amdgcn_s_sleep(1);
-            if (wall_clock64() - t0 > kWaitTicks) {
-                __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-        }
-    }
-    __syncthreads();
-
     // ---------------- fold: A[j] = gamma A[j] + sum_h p_hj ----------------
-    // global (max, sum) of this wave's heads: lane (q4, r16) reads head hh,
-    // chunks q4 + 4 hi + 8 k; the eight lanes of a head then merge.
+    // The chunk's old scores are loaded first, so their latency overlaps the
+    // wait for the statistics.
+    constexpr int KPT = (CHUNK + 64 * NW - 1) / (64 * NW);  // keys per thread
+    float* lsc = score + l * cap;
+    float a_old[KPT];
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+        const int k = tid + 64 * NW * i;
+        const int j = k_begin + k;
+        a_old[i] = (k < nk && j < len) ? lsc[j] : 0.f;
+    }
+    // Global (max, sum) of this wave's heads: lane (q4, hi, hh) polls head hh
+    // over chunks q4 + 4 hi + 8 k, 64 chunks per round, until no pair of the
+    // round is unpublished; the eight lanes of a head then merge.
     float m_h = -INFINITY, l_h = 0.f;
     {
         const float2* hrow = part_ml + l * nc_max * Hq + g * G + (hh < G ? hh : 0);
-        for (int c0 = q4 + 4 * hi; c0 < n_chunks; c0 += 32) {
-            float2 v[4];
+        const uint64_t t0 = wall_clock64();
+        for (int base = 0; base < n_chunks; base += 64) {
+            float2 v[8];
+            for (;;) {
+                bool ready = true;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int cc = c0 + 8 * k;
-                v[k] = ld_dev2(hrow + (cc < n_chunks ? cc : c0) * Hq);
-                if (cc >= n_chunks) v[k] = make_float2(-INFINITY, 0.f);
+                for (int k = 0; k < 8; ++k) {
+                    const int cc = base + q4 + 4 * hi + 8 * k;
+                    v[k] = cc < n_chunks ? ld_dev2(hrow + cc * Hq) : make_float2(-INFINITY, 1.f);
+                    ready = ready && v[k].y != 0.f;
+                }
+                if (__all(ready)) break;
+                if (wall_clock64() - t0 > kWaitTicks) {
+                    if (lane == 0) __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
             }
 #pragma unroll
-            for (int k = 0; k < 4; ++k) merge_ml(m_h, l_h, v[k].x, v[k].y);
+            for (int k = 0; k < 8; ++k) merge_ml(m_h, l_h, v[k].x, v[k].y);
         }
         merge_ml(m_h, l_h, __shfl_xor(m_h, 16, 64), __shfl_xor(l_h, 16, 64));
         merge_ml(m_h, l_h, __shfl_xor(m_h, 32, 64), __shfl_xor(l_h, 32, 64));
@@ -370,35 +374,29 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
         }
     }
     __syncthreads();
-    float* lsc = score + l * cap;
-    for (int k = tid; k < nk; k += 64 * NW) {
-        float a = 0.f;
 #pragma unroll
-        for (int gg = 0; gg < NW; ++gg) a += s_psum[gg][k];
-        const int j = k_begin + k;
-        lsc[j] = ((j < len) ? gamma * lsc[j] : 0.f) + a;
-    }
-
-    // ---------------- the last workgroup clears the counters ----------------
-    if (tid == 0) {
-        const uint32_t old = __hip_atomic_fetch_add(&hdr->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        if (old == static_cast<uint32_t>(n_items) - 1u) {
-            for (int ll = 0; ll < L; ++ll) __hip_atomic_store(&arrive[ll], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&hdr->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&hdr->done, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    for (int i = 0; i < KPT; ++i) {
+        const int k = tid + 64 * NW * i;
+        if (k < nk) {
+            float a = 0.f;
+#pragma unroll
+            for (int gg = 0; gg < NW; ++gg) a += s_psum[gg][k];
+            lsc[k_begin + k] = gamma * a_old[i] + a;  // a_old = 0 for the new slot (zero pad of Eq. 6)
         }
     }
 }
 
 // Combine kernel: one workgroup of D threads per (layer, head):
 //   o_h = sum_c O_c,h exp2(m_c,h - m_h) / l_h over the layer's chunks.
-__global__ __launch_bounds__(D) void decode_combine_kernel(const uint8_t* __restrict__ ws, uint16_t* __restrict__ out,
+// It then zeroes the (max, sum) pairs it has read (and workgroup (0, 0) the
+// ticket): the attend kernel of the next call starts from a clean workspace.
+__global__ __launch_bounds__(D) void decode_combine_kernel(uint8_t* __restrict__ ws, uint16_t* __restrict__ out,
                                                            int32_t Hq, int32_t n_chunks, int32_t nc_max, int32_t L,
                                                            int32_t hdr_bytes) {
     __shared__ float s_w[256];
     __shared__ float s_m, s_l;
     const int h = blockIdx.x, l = blockIdx.y, tid = threadIdx.x;
-    const float2* ml = reinterpret_cast<const float2*>(ws + hdr_bytes) + l * nc_max * Hq + h;
+    float2* ml = reinterpret_cast<float2*>(ws + hdr_bytes) + l * nc_max * Hq + h;
     const float* po = reinterpret_cast<const float*>(ws + hdr_bytes) + 2 * L * nc_max * Hq + (l * nc_max * Hq + h) * D;
     if (tid < 64) {  // wave 0: global (max, sum) of the head over the chunks
         float m = -INFINITY, s = 0.f;
@@ -417,6 +415,8 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const uint8_t* __rest
     const float m = s_m, inv_l = 1.0f / s_l;
     for (int cc = tid; cc < n_chunks; cc += D) s_w[cc] = exp2f(ml[cc * Hq].x - m) * inv_l;
     __syncthreads();
+    for (int cc = tid; cc < n_chunks; cc += D) ml[cc * Hq] = make_float2(0.f, 0.f);
+    if (h == 0 && l == 0 && tid == 0) reinterpret_cast<WsHeader*>(ws)->ticket = 0u;
     float acc = 0.f;
 #pragma unroll 8
     for (int cc = 0; cc < n_chunks; ++cc) acc += s_w[cc] * po[cc * Hq * D + tid];
@@ -427,8 +427,8 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(const uint8_t* __rest
 
 // ---- sizing shared with the host API ----
 size_t vz_decode_hdr_bytes(int32_t L) {
-    const size_t b = sizeof(WsHeader) + sizeof(uint32_t) * static_cast<size_t>(L);
-    return (b + 255) & ~static_cast<size_t>(255);
+    (void)L;
+    return sizeof(WsHeader);
 }
 
 int32_t vz_decode_fused_chunks(int32_t T) { return (T + CHUNK - 1) / CHUNK; }

@@ -141,8 +141,8 @@ hipError_t vz_launch_fuse(const void* k_in, const void* v_in, int32_t T_in, cons
                           float* score_out, int32_t* pos_out, int32_t L, int32_t H, int32_t d,
                           int32_t cap_out, int32_t dtype, hipStream_t stream);
 size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap);
-// decode workspace: a header (ticket, done, error, per-layer arrival counters)
-// of vz_decode_hdr_bytes(L) bytes, then path-specific scratch
+// decode workspace: a header (ticket, error flag) of vz_decode_hdr_bytes(L)
+// bytes, then path-specific scratch
 size_t vz_decode_hdr_bytes(int32_t L);
 bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap, int32_t L);
 size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
