@@ -257,6 +257,7 @@ int orc_evict_select(const double *score, const int32_t *pos, int32_t len,
 typedef struct {
     int64_t s, e;
     int32_t lt;
+    int32_t idx; /* input order, the last tie-break: the order is total */
 } orc_seg;
 
 static int seg_by_start(const void *a, const void *b)
@@ -264,14 +265,16 @@ static int seg_by_start(const void *a, const void *b)
     const orc_seg *x = (const orc_seg *)a, *y = (const orc_seg *)b;
     if (x->s != y->s)
         return (x->s > y->s) - (x->s < y->s);
-    return (x->e > y->e) - (x->e < y->e);
+    if (x->e != y->e)
+        return (x->e > y->e) - (x->e < y->e);
+    return (x->idx > y->idx) - (x->idx < y->idx);
 }
 
 /* Span offsets for the compressed sequence of Eq. (5).
  * Segments with confidence above the threshold are kept; Eq. (3) maps each
  * timestamp to floor(L_a * tau / tau_total) (exact in 64-bit integers);
- * segments are taken in start order, a start inside the previous segment is
- * moved to its end, empty ones are dropped.  A semantic interval [s, e) of
+ * segments are taken in start order (then end, then input order), a start
+ * inside the previous segment is moved to its end, empty ones are dropped.  A semantic interval [s, e) of
  * length n becomes g = min(L_t, n) groups; every uncovered token is a
  * background span of length 1.  off_out needs room for L_a + 1 entries. */
 int orc_build_offsets(const int64_t *t_start_ms, const int64_t *t_end_ms,
@@ -294,7 +297,7 @@ int orc_build_offsets(const int64_t *t_start_ms, const int64_t *t_end_ms,
         if (te <= ts)
             continue;
         orc_seg sg = {((int64_t)L_a * ts) / t_total_ms, ((int64_t)L_a * te) / t_total_ms,
-                      text_len[i]};
+                      text_len[i], i};
         seg[n++] = sg;
     }
     qsort(seg, (size_t)n, sizeof(orc_seg), seg_by_start);

@@ -24,11 +24,11 @@ def _labels(ts, te, conf, tl, t_total, L_a, thr=0.3):
             continue
         i0 = int(Fraction(L_a) * Fraction(int(s), int(t_total)))  # floor for non-negatives
         i1 = int(Fraction(L_a) * Fraction(int(e), int(t_total)))
-        segs.append((i0, i1, n))
-    segs.sort()
+        segs.append((i0, i1, len(segs), n))
+    segs.sort()  # start, then end, then input order
     owner = [None] * L_a
     cur = 0
-    for idx, (i0, i1, n) in enumerate(segs):
+    for idx, (i0, i1, _, n) in enumerate(segs):
         i0 = max(i0, cur)
         if i1 <= i0 or n < 1:
             continue
@@ -94,3 +94,13 @@ def test_overlaps_are_clipped_and_text_longer_than_audio():
                                [50, 1], 2000, 20)
     # first: tokens 0..9 with 50 text tokens -> min(50, 10) = 10 groups of 1; second: 10..19 -> 1 group
     assert off.tolist() == list(range(11)) + [20]
+
+
+def test_equal_intervals_keep_input_order():
+    # two segments mapping to the same token interval: the first one in input
+    # order is taken, the second starts at its end and is dropped (empty)
+    conf = np.array([0.9, 0.9], np.float32)
+    off = oracle.build_offsets([0, 0], [1000, 1000], conf, [2, 5], 1000, 8)
+    assert off.tolist() == [0, 4, 8]
+    off = oracle.build_offsets([0, 0], [1000, 1000], conf, [5, 2], 1000, 8)
+    assert off.tolist() == [0, 1, 3, 4, 6, 8]
