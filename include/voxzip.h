@@ -55,6 +55,34 @@ extern "C" {
 #define VZ_OP_EVICT 2
 
 /*
+ * Stage-1 span offsets (Sec. 3.2.1: confidence filter, Eq. 3 time-to-token
+ * map, uniform partition of each semantic interval into groups, background
+ * tokens kept one per span).  Host function: every pointer is a host pointer.
+ *
+ *  t_start_ms, t_end_ms  int64 [n_seg] segment times in ms (clipped to
+ *               [0, t_total_ms]); conf float32 [n_seg]; text_len int32 [n_seg]
+ *               (text tokens of each segment).
+ *  t_total_ms   duration of the audio, > 0; L_a audio tokens, >= 0.
+ *  conf_threshold  a segment is used when conf > conf_threshold (0.3 in the paper).
+ *  off_out      int32 [L_a + 1] (room for the worst case): receives span_off
+ *               for voxzip_fuse_spans, off_out[0] = 0, strictly increasing,
+ *               off_out[*n_spans_out] = L_a.
+ *  n_spans_out  receives the number of spans.
+ * A segment covers tokens [floor(L_a t_start / t_total), floor(L_a t_end /
+ * t_total)) (exact integer arithmetic).  Segments are taken in the order
+ * (first token, last token, input order); a segment starting inside tokens
+ * already covered starts where they end; an empty interval, or a segment
+ * with text_len < 1, is skipped.  An interval of n tokens becomes
+ * g = min(text_len, n) groups with boundaries first + floor(j n / g).
+ * Errors: VZ_ERR_INVALID for null pointers, n_seg < 0, t_total_ms <= 0,
+ * L_a < 0 or L_a * t_total_ms beyond int64.
+ */
+VZ_API int voxzip_build_span_offsets(const int64_t *t_start_ms, const int64_t *t_end_ms,
+                                     const float *conf, const int32_t *text_len, int32_t n_seg,
+                                     int64_t t_total_ms, int32_t L_a, float conf_threshold,
+                                     int32_t *off_out, int32_t *n_spans_out);
+
+/*
  * Stage-1 semantic-anchored fusion (Sec. 3.2.1, Eq. 4 group average pooling,
  * the additive text anchor that follows it, and the chronological
  * concatenation of Eq. 5), applied to each layer's K and V per KV head.

@@ -43,6 +43,8 @@ def lib() -> ctypes.CDLL:
                                              i32, i32, i32, i32, i32, i32, P, sz, P]
     L.voxzip_evict_compact.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, P, P,
                                        i32, i32, i32, i32, i32, P, sz, P]
+    L.voxzip_build_span_offsets.argtypes = [P, P, P, P, i32, ctypes.c_int64, i32, f32, P, P]
+    L.voxzip_build_span_offsets.restype = ctypes.c_int
     L.voxzip_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
     L.voxzip_workspace_bytes.restype = sz
     for f in (L.voxzip_fuse_spans, L.voxzip_decode_attend_score, L.voxzip_evict_compact):
@@ -85,6 +87,26 @@ def _stream(stream):
     import torch
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def voxzip_build_span_offsets(t_start_ms, t_end_ms, conf, text_len, t_total_ms: int, L_a: int,
+                              conf_threshold: float = 0.3):
+    """Stage-1 span offsets on the host (numpy arrays in, int32 offsets out:
+    n_spans + 1 entries, ready for voxzip_fuse_spans once copied to the GPU)."""
+    import numpy as np
+    ts = np.ascontiguousarray(t_start_ms, dtype=np.int64)
+    te = np.ascontiguousarray(t_end_ms, dtype=np.int64)
+    cf = np.ascontiguousarray(conf, dtype=np.float32)
+    tl = np.ascontiguousarray(text_len, dtype=np.int32)
+    n_seg = len(ts)
+    if not (len(te) == len(cf) == len(tl) == n_seg):
+        raise ValueError("segment arrays differ in length")
+    off = np.zeros(max(int(L_a), 0) + 1, dtype=np.int32)
+    n = np.zeros(1, dtype=np.int32)
+    hp = lambda a: ctypes.c_void_p(a.ctypes.data)
+    _check(lib().voxzip_build_span_offsets(hp(ts), hp(te), hp(cf), hp(tl), n_seg, int(t_total_ms), int(L_a),
+                                           float(conf_threshold), hp(off), hp(n)))
+    return off[: int(n[0]) + 1].copy()
 
 
 def voxzip_workspace_bytes(op: int, n_layers: int, n_q_heads: int, kv_heads: int, d: int, cap: int) -> int:

@@ -69,6 +69,21 @@ size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_heads, i
     return 0;
 }
 
+int voxzip_build_span_offsets(const int64_t* t_start_ms, const int64_t* t_end_ms, const float* conf,
+                              const int32_t* text_len, int32_t n_seg, int64_t t_total_ms, int32_t L_a,
+                              float conf_threshold, int32_t* off_out, int32_t* n_spans_out) {
+    static const char* fn = "voxzip_build_span_offsets";
+    if (!off_out || !n_spans_out) return fail(VZ_ERR_INVALID, fn, "null output pointer");
+    if (n_seg < 0 || t_total_ms <= 0 || L_a < 0)
+        return fail(VZ_ERR_INVALID, fn, "n_seg and L_a must be >= 0 and t_total_ms > 0");
+    if (n_seg > 0 && (!t_start_ms || !t_end_ms || !conf || !text_len))
+        return fail(VZ_ERR_INVALID, fn, "null segment array");
+    if (L_a > 0 && t_total_ms > INT64_MAX / L_a) return fail(VZ_ERR_INVALID, fn, "L_a * t_total_ms overflows");
+    *n_spans_out = vz_build_span_offsets(t_start_ms, t_end_ms, conf, text_len, n_seg, t_total_ms, L_a,
+                                         conf_threshold, off_out);
+    return VZ_OK;
+}
+
 int voxzip_fuse_spans(const void* k_in, const void* v_in, int32_t T_in, const int32_t* span_off, int32_t n_spans,
                       const void* anchor_k, const void* anchor_v, void* k_out, void* v_out, float* score_out,
                       int32_t* pos_out, int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap_out,

@@ -136,6 +136,11 @@ struct VzEvictArgs {
     void* ws; size_t ws_bytes;
 };
 
+// Stage-1 span offsets (host); arguments checked by the caller; returns the
+// number of spans written to off_out[1..].
+int32_t vz_build_span_offsets(const int64_t* t_start_ms, const int64_t* t_end_ms, const float* conf,
+                              const int32_t* text_len, int32_t n_seg, int64_t t_total_ms, int32_t L_a,
+                              float conf_threshold, int32_t* off_out);
 hipError_t vz_launch_fuse(const void* k_in, const void* v_in, int32_t T_in, const int32_t* off,
                           int32_t n_spans, const void* ak, const void* av, void* k_out, void* v_out,
                           float* score_out, int32_t* pos_out, int32_t L, int32_t H, int32_t d,

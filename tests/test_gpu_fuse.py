@@ -93,3 +93,23 @@ def test_fuse_full_size_sampled_layers():
     for l in (0, 23, 47):
         _verify(k_in[l:l + 1], v_in[l:l + 1], off, w.dtype, k[l:l + 1], v[l:l + 1], s[l:l + 1], p[l:l + 1], sen)
     assert np.all(p[:, :n] == np.arange(n)) and np.all(s[:, :n] == 0)
+
+
+def test_fuse_with_offsets_from_the_span_builder():
+    """End to end Stage 1: ASR segments -> voxzip_build_span_offsets (host) ->
+    voxzip_fuse_spans (GPU), against the oracle's fusion of the oracle's offsets."""
+    import paper_2608_08569_amd as vz
+    key = synth.stream_key(5, "stage1-e2e")
+    r = synth.uniform01(key, 0, 256)
+    t_total, L_a, n = 120000, 1500, 30
+    starts = np.sort((r[:n] * (t_total - 5000)).astype(np.int64))
+    ends = starts + 800 + (r[n:2 * n] * 4000).astype(np.int64)
+    conf = (0.1 + 0.9 * r[2 * n:3 * n]).astype(np.float32)
+    tl = 1 + (r[3 * n:4 * n] * 12).astype(np.int32)
+    off = vz.voxzip_build_span_offsets(starts, ends, conf, tl, t_total, L_a)
+    assert np.array_equal(off, oracle.build_offsets(starts, ends, conf, tl, t_total, L_a))
+    dtype, L, H, d = synth.DT_BF16, 2, 4, 128
+    x = synth.as_storage(synth.normal_f32(synth.stream_key(key, "k"), L * H * L_a * d).reshape(L, H, L_a, d), dtype)
+    y = synth.as_storage(synth.normal_f32(synth.stream_key(key, "v"), L * H * L_a * d).reshape(L, H, L_a, d), dtype)
+    _, k, v, s, p, sen = _run(x, y, off, dtype, len(off) + 7)
+    _verify(x, y, off, dtype, k, v, s, p, sen)

@@ -1,0 +1,73 @@
+"""The library's Stage-1 span builder (voxzip_build_span_offsets, host code)
+against the oracle's, bit for bit (Sec. 3.2.1: confidence filter, Eq. 3,
+uniform groups, background tokens).  Runs on the CPU."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+vz = pytest.importorskip("paper_2608_08569_amd")
+
+
+def _both(ts, te, conf, tl, t_total, L_a, thr=0.3):
+    ref = oracle.build_offsets(ts, te, conf, tl, t_total, L_a, thr)
+    got = vz.voxzip_build_span_offsets(ts, te, conf, tl, t_total, L_a, thr)
+    assert np.array_equal(got, ref), (got.tolist(), ref.tolist())
+    return got
+
+
+def _random_case(seed, n_max, la_max):
+    key = synth.stream_key(seed, "spans-product")
+    r = synth.uniform01(key, 0, 8 * n_max + 8)
+    L_a = int(r[0] * la_max)
+    t_total = 1 + int(r[1] * 600000)
+    n = int(r[2] * n_max)
+    ts = (r[8:8 + n] * 1.2 * t_total - 0.1 * t_total).astype(np.int64)       # some before 0
+    te = ts + (r[8 + n:8 + 2 * n] * 0.5 * t_total - 0.05 * t_total).astype(np.int64)  # some empty or reversed
+    conf = r[8 + 2 * n:8 + 3 * n].astype(np.float32)
+    tl = (r[8 + 3 * n:8 + 4 * n] * 40).astype(np.int32) - 2                 # includes 0 and negatives
+    # exact duplicates of earlier segments (equal token intervals, other text lengths)
+    if n > 3:
+        ts[n - 1], te[n - 1] = ts[0], te[0]
+    return ts, te, conf, tl, t_total, L_a
+
+
+@pytest.mark.parametrize("seed", range(200))
+def test_random_segment_lists_match_the_oracle(seed):
+    _both(*_random_case(seed, n_max=24, la_max=400))
+
+
+def test_five_minutes_of_speech():
+    # 5 min at 12.5 audio tokens/s with 60 ASR segments of a few seconds each
+    key = synth.stream_key(3, "spans-speech")
+    r = synth.uniform01(key, 0, 256)
+    t_total, L_a, n = 300000, 3750, 60
+    starts = np.sort((r[:n] * (t_total - 6000)).astype(np.int64))
+    ends = starts + 1000 + (r[n:2 * n] * 5000).astype(np.int64)
+    conf = (0.2 + 0.8 * r[2 * n:3 * n]).astype(np.float32)
+    tl = 2 + (r[3 * n:4 * n] * 20).astype(np.int32)
+    off = _both(starts, ends, conf, tl, t_total, L_a)
+    assert off[0] == 0 and off[-1] == L_a and np.all(np.diff(off) > 0)
+
+
+def test_worked_cases():
+    c9 = np.array([0.9], np.float32)
+    assert _both([10000], [20000], c9, [25], 40000, 400).size == 100 + 25 + 200 + 1
+    assert _both([0], [1000], np.array([0.3], np.float32), [2], 1000, 8).tolist() == list(range(9))
+    two = np.array([0.9, 0.9], np.float32)
+    assert _both([0, 0], [1000, 1000], two, [2, 5], 1000, 8).tolist() == [0, 4, 8]
+    assert _both([0, 0], [1000, 1000], two, [5, 2], 1000, 8).tolist() == [0, 1, 3, 4, 6, 8]
+    assert _both([], [], np.array([], np.float32), [], 1000, 5).tolist() == [0, 1, 2, 3, 4, 5]
+    assert _both([], [], np.array([], np.float32), [], 1000, 0).tolist() == [0]
+
+
+@pytest.mark.parametrize("args", [
+    dict(t_total_ms=0, L_a=8),
+    dict(t_total_ms=-5, L_a=8),
+    dict(t_total_ms=1000, L_a=-1),
+    dict(t_total_ms=2 ** 62, L_a=8),          # L_a * t_total_ms beyond int64
+])
+def test_invalid_arguments_are_rejected(args):
+    with pytest.raises(vz.VoxzipError):
+        vz.voxzip_build_span_offsets([0], [10], np.array([0.9], np.float32), [1], **args)
