@@ -247,6 +247,23 @@ def workload(name: str, seed: int = 0) -> Workload:
     raise KeyError(name)
 
 
+BATCH = 16  # sequences of the batched-decode workload
+
+
+def batch_lengths(seed: int = 0) -> np.ndarray:
+    """Audio tokens of the 16 sequences of the batched workload, iid uniform on {2048..32768}."""
+    return uniform_int(stream_key(seed, "batch16", "lengths"), 0, BATCH, 2048, 32768).astype(np.int64)
+
+
+def batch_workloads(seed: int = 0) -> list:
+    """One Workload per sequence of the batched workload: 48 layers, 32Q/4KV,
+    d = 128, bf16, spans of mean length 4 (as "layer"), budget len / 4 of the
+    sequence's audio tokens, eviction every 16 steps, 128 steps.  The sequence
+    index (0..15) is the ``seq`` argument of the per-sequence generators."""
+    return [Workload("batch16", 48, 32, 4, 128, DT_BF16, int(n), 0, "geom4", 0.95, int(n) // 4, 128,
+                     interval=16, seed=seed) for n in batch_lengths(seed)]
+
+
 def span_lengths(w: Workload, seq: int = 0) -> np.ndarray:
     key = stream_key(w.seed, w.name, "spans", seq)
     if w.span_kind == "uniform":

@@ -170,3 +170,39 @@ def test_long32k_full_size_sampled_layers():
     g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
     _run_workload(w, g, 6, layers=[0, 47])
     assert g.len == min(n + 6, w.budget) or g.len == w.budget
+
+
+def test_aggr64k_full_size_sampled_layers():
+    """The 48-layer 64k-token workload at full size (20x compression, queries
+    biased towards ~5% of the keys): 65,536 tokens fused into ~13.1k spans; the
+    first eviction removes ~9.8k rows per layer (radix select, grid-wide
+    compaction), the later ones one row; layers 0 and 47 are checked against
+    the oracle every step."""
+    w = synth.workload("aggr64k")
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n = len(off) - 1
+    cap = max(n, w.budget) + 32
+    g = GpuCache(w.n_layers, w.n_q_heads, w.kv_heads, w.d, cap, w.dtype)
+    g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
+    _run_workload(w, g, 4, layers=[0, 47])
+    assert g.len == w.budget
+
+
+def test_batch16_per_sequence_calls():
+    """The batched workload, one call sequence per sequence (16 caches of 2k-32k
+    audio tokens, budget len/4, eviction every 16 steps), on the first 2 of the
+    48 layers at the real head shape; every sequence is checked against the
+    oracle every step for 32 steps (two evictions of ~16 rows each)."""
+    layers = range(2)
+    for i, w in enumerate(synth.batch_workloads()):
+        off = synth.offsets_from_lengths(synth.span_lengths(w, seq=i))
+        n = len(off) - 1
+        g = GpuCache(len(layers), w.n_q_heads, w.kv_heads, w.d, max(n, w.budget) + 17, w.dtype)
+        g.fuse(to_dev(synth.prefill_kv(w, "k", seq=i, layers=layers)),
+               to_dev(synth.prefill_kv(w, "v", seq=i, layers=layers)), to_dev(off))
+        for t in range(32):
+            q, kn, vn = synth.decode_inputs(w, t, seq=i)
+            ref_s, state = synced_step(g, q[:2], kn[:2], vn[:2], w.gamma)
+            if (t + 1) % w.interval == 0 and g.len > w.budget:
+                synced_evict(g, ref_s, state, w.budget)
+        assert g.len == min(n + 32, w.budget)

@@ -122,3 +122,16 @@ def test_decode_inputs_shapes_and_bias():
     assert np.allclose(norms, norms[0, 0])
     q, k, v = synth.decode_inputs(w, 0, bias=b)
     assert q.shape == (2, 32, 128) and k.shape == (2, 4, 128) and q.dtype == np.uint16
+
+
+def test_batch_workload():
+    lens = synth.batch_lengths()
+    assert lens.shape == (synth.BATCH,) and lens.min() >= 2048 and lens.max() <= 32768
+    assert np.array_equal(lens, synth.batch_lengths())            # seeded
+    assert not np.array_equal(lens, synth.batch_lengths(seed=1))
+    ws = synth.batch_workloads()
+    assert [w.budget for w in ws] == [int(n) // 4 for n in lens]
+    assert all(w.interval == 16 and w.n_layers == 48 and w.steps == 128 for w in ws)
+    # each sequence draws its own spans
+    a, b = synth.span_lengths(ws[0], seq=0), synth.span_lengths(ws[1], seq=1)
+    assert a.sum() == lens[0] and b.sum() == lens[1] and not np.array_equal(a[:50], b[:50])
