@@ -111,6 +111,120 @@ def cpu_baseline(w, n_layers_sample: int, max_seconds: float):
     }
 
 
+class Sequence:
+    """One sequence of a workload on its own stream: span structure from the
+    seeded generator, K/V and per-step q/k/v drawn on the GPU from a seeded
+    torch generator (N(0,1), plus the workload's query bias), cache and
+    workspaces sized as in the parity tests."""
+
+    def __init__(self, torch, vz, w, seq, steps, stream):
+        self.vz, self.w, self.stream = vz, w, stream
+        L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(synth.stream_key(w.seed, w.name, "bench", seq) & 0x7FFFFFFFFFFFFFFF)
+        off = synth.offsets_from_lengths(synth.span_lengths(w, seq=seq))
+        self.n = len(off) - 1
+        T_in = w.n_audio + w.n_text
+        bf = torch.bfloat16
+        rn = lambda *shape: torch.randn(*shape, generator=gen, device="cuda", dtype=torch.float32).to(bf)
+        self.k_in, self.v_in = rn(L, Hkv, T_in, d), rn(L, Hkv, T_in, d)
+        self.off = torch.from_numpy(off).cuda()
+        bias = torch.from_numpy(synth.q_bias(w)).to("cuda", torch.float32) if w.q_bias else None
+        self.steps_in = []
+        for _ in range(steps):
+            q = torch.randn(L, Hq, d, generator=gen, device="cuda")
+            q = (q + bias if bias is not None else q).to(bf)
+            self.steps_in.append((q, rn(L, Hkv, d), rn(L, Hkv, d)))
+        self.cap = max(self.n, w.budget) + w.interval + 1
+        self.K = torch.zeros(L, Hkv, self.cap, d, dtype=bf, device="cuda")
+        self.V = torch.zeros_like(self.K)
+        self.S = torch.zeros(L, self.cap, dtype=torch.float32, device="cuda")
+        self.P = torch.zeros(L, self.cap, dtype=torch.int32, device="cuda")
+        self.out = torch.zeros(L, Hq, d, dtype=bf, device="cuda")
+        self.ws_d = vz.workspace(vz.VZ_OP_DECODE, L, Hq, Hkv, d, self.cap)
+        self.ws_e = vz.workspace(vz.VZ_OP_EVICT, L, Hq, Hkv, d, self.cap)
+
+    def start(self):
+        self.vz.voxzip_fuse_spans(self.k_in, self.v_in, self.off, self.K, self.V, self.S, self.P,
+                                  stream=self.stream)
+        self.len = self.nxt = self.n
+        return 0
+
+    def step(self, t):
+        """Decode step t (and the eviction when it is due); returns algorithmic bytes."""
+        w, vz = self.w, self.vz
+        L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+        q, kn, vn = self.steps_in[t]
+        vz.voxzip_decode_attend_score(q, kn, vn, self.K, self.V, self.S, self.P, self.out, self.len, self.nxt,
+                                      w.gamma, workspace=self.ws_d, stream=self.stream)
+        T = self.len + 1
+        b = L * decode_bytes_per_layer(T, Hq, Hkv, d, 2)
+        self.len, self.nxt = T, self.nxt + 1
+        if (t + 1) % w.interval == 0 and self.len > w.budget:
+            E = self.len - w.budget
+            self.len = vz.voxzip_evict_compact(self.K, self.V, self.S, self.P, self.len, w.budget, self.nxt,
+                                               workspace=self.ws_e, stream=self.stream)
+            b += L * evict_bytes_per_layer(T, E, Hkv, d, 2)
+        return b
+
+
+def other_workload(args, torch, vz):
+    """aggr64k (one sequence, 512 steps) or batch16 (16 sequences of 2k-32k
+    tokens on 16 streams, 128 steps each, eviction every 16 steps): whole
+    requests (fusion + all steps), tokens/s over the wall clock and the
+    algorithmic bytes of the path per second."""
+    if args.workload == "aggr64k":
+        ws_ = [synth.workload("aggr64k")]
+    else:
+        ws_ = synth.batch_workloads()
+    steps = ws_[0].steps
+    t0 = time.time()
+    seqs = [Sequence(torch, vz, w, i, steps, torch.cuda.Stream()) for i, w in enumerate(ws_)]
+    torch.cuda.synchronize()
+    log(f"[gpu] {args.workload}: {len(seqs)} sequence(s), {sum(s.n for s in seqs)} spans, "
+        f"inputs ready in {time.time() - t0:.1f}s")
+
+    def request():
+        b = 0
+        for s in seqs:
+            s.start()
+        for t in range(steps):
+            for s in seqs:
+                b += s.step(t)
+        return len(seqs) * steps, b
+
+    for _ in range(args.warmup):
+        request()
+    torch.cuda.synchronize()
+    tokens = path_bytes = 0
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        tk, b = request()
+        tokens += tk
+        path_bytes += b
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    w = ws_[0]
+    if args.workload == "aggr64k":
+        desc = (f"48 layers, 32Q/4KV, d=128, bf16; 65536 audio tokens (spans of mean length 5, 10 percent of "
+                f"length 1) fused to {seqs[0].n} spans, B=3277, queries biased to about 5 percent of the keys, "
+                f"512 decode steps with eviction")
+    else:
+        lens = "/".join(str(s.w.n_audio) for s in seqs)
+        desc = (f"16 sequences of {lens} audio tokens (spans of mean length 4), budget len/4 each, eviction "
+                f"every 16 steps, 128 decode steps each; one HIP stream per sequence")
+    print(json.dumps({
+        "metric": "decode attend+score+evict tokens/s and HBM GB/s (% of peak)",
+        "value": tokens / elapsed, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "description": desc, "layers": w.n_layers,
+                   "sequences": len(seqs), "decode_steps_per_request": steps},
+        "path_gbps": path_bytes / elapsed / 1e9,
+        "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,6 +236,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
+    ap.add_argument("--workload", default="long32k", choices=["long32k", "aggr64k", "batch16"],
+                    help="long32k is the headline; the others are reported beside it")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -144,6 +260,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n}))
+        return
+
+    if args.workload != "long32k":
+        other_workload(args, torch, vz)
         return
 
     w = synth.workload("long32k")
@@ -254,8 +374,8 @@ def main():
         "fuse_ms_mean": float(np.mean(fuse_ms)),
         "fuse_gbps": fuse_bytes / (float(np.mean(fuse_ms)) * 1e-3) / 1e9,
         "roofline": {
-            "kernel": ("voxzip_decode_attend_score = decode_attend_kernel + decode_combine_kernel "
-                       "(48 layers, T=8193)"),
+            "kernel": ("voxzip_decode_attend_score = decode_attend_kernel + decode_output_kernel + "
+                       "decode_fold_kernel (48 layers, T=8193)"),
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,

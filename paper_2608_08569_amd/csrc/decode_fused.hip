@@ -1,50 +1,39 @@
 // Decode step (Sec. 3.1 Eq. 1-2, Sec. 3.2.2 Eq. 6) for bfloat16 caches with
-// d = 128 and at most 8 query heads per KV head.  Two launches cover every
-// layer: the attend kernel (attention on the matrix cores and the
-// decayed-score fold from registers) and a small combine kernel (the output
-// rows from the per-chunk partials).
+// d = 128 and at most 8 query heads per KV head.  Three launches cover every
+// layer: the attend kernel streams the cache once and leaves per-chunk
+// partial results in the workspace; the output and fold kernels merge them
+// into the output rows and the decayed scores.  No workgroup ever waits for
+// another.
 //
-// Attend kernel: work item = (layer, key chunk of <= 256 keys).  A workgroup
+// Attend kernel: work item = (layer, key chunk of <= 128 keys).  A workgroup
 // has one wave per KV head; wave g streams K and V rows of head g over the
-// chunk:
+// chunk.  Registers stay under 128 per lane so that four workgroups share a
+// CU.
 //   pass 1  S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (M = 16 keys, N = 16
 //           query-head columns of which n_q/n_kv <= 8 are used, K = 32
 //           channels).  K tiles of 32 rows are loaded fully coalesced (4 whole
-//           rows per 1 KB instruction), stored to LDS with an XOR swizzle on
-//           the row index, and read back with ds_read_b128 in the A-operand
-//           layout, bank-conflict free.  One tile is in flight while the
-//           previous one is multiplied.  The logits of an odd 16-key tile are
+//           rows per 1 KB instruction), stored to LDS with padded rows and
+//           read back with ds_read_b128 in the A-operand layout.  One tile is
+//           in flight while the previous one is multiplied; the first V tile
+//           follows the last K tile.  The logits of an odd 16-key tile are
 //           moved into the unused head columns 8..15 of the even tile's
-//           registers (DPP row rotate by 8), so 256 keys x 8 heads take 32
+//           registers (DPP row rotate by 8), so 128 keys x 8 heads take 16
 //           registers per lane.
-//   stats   chunk-local max and sum per head; the registers then hold
-//           p~ = exp(s - m_chunk).  Each (max, sum) pair is published to the
-//           workspace at once with one 64-bit store; a sum is at least 1 for
-//           a non-empty chunk, so a zero sum marks a pair not yet published.
-//   pass 2  O += P V: V tiles of 32 keys take the same coalesced path into
-//           LDS (another swizzle) and are read back with ds_read_b64_tr_b16
-//           directly in the B-operand layout; P is rebuilt from the packed p~
-//           registers with one row rotate.  The partial O goes to the
-//           workspace for the combine kernel.
-//   fold    by now the other chunks of the layer have normally published
-//           their statistics too (the wait is for their pass 1 only); each
-//           wave polls the pairs of its own heads until none is zero, merges
-//           them into the layer's (max, sum) per head and folds
-//               A[j] = gamma * A[j] + sum_h exp(s_hj - m_h) / l_h
-//           for its own keys from the p~ still in registers -- no logit ever
-//           goes to HBM.
-// Work items are taken in ticket order (one atomic per workgroup), so the
-// chunks of a layer start together whatever order the hardware dispatches
-// workgroups in.  A chunk waits only for chunks of its layer that already
-// hold a ticket and never wait themselves before publishing, and the number
-// of chunks per layer is kept below the number of workgroups that can be
-// resident, so every wait ends; it is also bounded in time (on expiry the
-// kernel flags an error in the workspace and finishes).  Statistics move
-// through device-scope atomic stores and loads, coherent across the per-XCD
-// L2 caches, so no cache-wide flush is needed.  The combine kernel, which
-// runs after every attend workgroup has finished, zeroes the pairs it has
-// read and the ticket, so the workspace is ready for the next call.
+//   stats   chunk-local max m_c and sum l_c of exp2 per head; the registers
+//           then hold p~ = exp2(s - m_c).  (m_c, l_c) and p~ (half precision,
+//           64 bytes per key over the 32 heads of the workload) go to the
+//           workspace.
+//   pass 2  O_c = P V: V tiles take the same coalesced path into LDS and are
+//           read back with ds_read_b64_tr_b16 directly in the B-operand
+//           layout; P is rebuilt from the packed p~ registers with one row
+//           rotate.  O_c (relative to m_c) goes to the workspace in bfloat16.
+// Output kernel: per (head, layer), the output row merged from the chunk
+// partials, and the layer's (max, sum) of the head.  Fold kernel: per (chunk,
+// layer), the chunk's scores A[j] = gamma A[j] + sum_h p_hj from p~ and one
+// factor per head.
 #include <math.h>
+
+#include <type_traits>
 
 #include "vz_internal.h"
 
@@ -56,22 +45,62 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int D = 128;
 constexpr int GMAX = 8;                // query heads per KV head served here
-constexpr int TILES = 16;              // 16-key MFMA tiles per chunk
+constexpr int TILES = 8;               // 16-key MFMA tiles per chunk
 constexpr int PAIRS = TILES / 2;       // packed tile pairs = 32-key tiles
 constexpr int CHUNK = 16 * TILES;      // keys per chunk (at most)
 constexpr int VT = 32;                 // keys per staged tile
 constexpr int KSTEPS = D / 32;         // MFMA k-steps over the channels
 constexpr int DTILES = D / 16;         // output column tiles
+constexpr int MAX_CHUNKS = 512;        // chunks per layer served here
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr uint64_t kWaitTicks = 20000000ull;  // 0.2 s of the 100 MHz constant clock
 constexpr int kRor8 = 0x128;           // DPP row_ror:8 (swap the halves of each 16-lane row)
 constexpr int kBufferDword3 = 0x00020000;  // raw buffer descriptor word 3 (32-bit data format)
 
-struct WsHeader {
-    uint32_t ticket;
-    uint32_t error;
-    uint32_t pad[62];
+// Staged tiles are 32 rows of 256 bytes with padded row strides, so that every
+// LDS address is one per-lane base plus an immediate (bank analysis in the
+// design notes): K rows 272 bytes apart (16 rows at one 16-byte column fall on
+// 16 distinct bank groups), V rows 288 bytes apart (4 rows x 32 bytes of a
+// transposed read fall on distinct banks).
+constexpr int KSTRIDE = 256 + 16;
+constexpr int VSTRIDE = 256 + 32;
+constexpr int TILE_BYTES = VT * VSTRIDE;
+
+constexpr size_t kHeaderBytes = 256;  // decode workspace header (unused by this path)
+
+// Per-chunk partial results in the workspace, after the header:
+//   ml [L][nc_max][Hq]        float2     chunk max m_c and sum l_c of exp2, per head
+//   o  [L][nc_max][Hq][D]     bfloat16   O_c relative to m_c
+//   p  [L][nc_max][Hq][CHUNK] half       p~ = exp2(s - m_c) per key of the chunk
+//   layer [L][Hq]             float2     the layer's max M and 1 / sum S, per head
+template <typename B>
+struct PartialsT {
+    using F2 = typename std::conditional<std::is_const<B>::value, const float2, float2>::type;
+    using U16 = typename std::conditional<std::is_const<B>::value, const uint16_t, uint16_t>::type;
+    F2* ml;
+    U16* o;
+    U16* p;
+    F2* layer;
+    __device__ PartialsT(B* ws, int hdr_bytes, int L, int nc_max, int Hq) {
+        const size_t n = static_cast<size_t>(L) * nc_max * Hq;
+        ml = reinterpret_cast<F2*>(ws + hdr_bytes);
+        o = reinterpret_cast<U16*>(ml + n);
+        p = o + n * D;
+        layer = reinterpret_cast<F2*>(p + n * CHUNK);
+    }
 };
+using Partials = PartialsT<uint8_t>;
+using ConstPartials = PartialsT<const uint8_t>;
+
+size_t partials_bytes(int32_t L, int32_t nc_max, int32_t Hq) {
+    return static_cast<size_t>(L) * nc_max * Hq * (sizeof(float2) + sizeof(uint16_t) * (D + CHUNK)) +
+           static_cast<size_t>(L) * Hq * sizeof(float2);
+}
+
+// First key of chunk c of T keys split into n near-equal chunks (c <= 512 and
+// T < 2^22, checked on the host, so the product fits in 32 bits).
+__host__ __device__ __forceinline__ int chunk_begin(int c, int T, int n) {
+    return static_cast<int>(static_cast<uint32_t>(c) * static_cast<uint32_t>(T) / static_cast<uint32_t>(n));
+}
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
     bf16x8_t r;
@@ -83,49 +112,31 @@ __device__ __forceinline__ float ror8(float v) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kRor8, 0xF, 0xF, false));
 }
 
-// Device-scope (all XCDs) coherent 64-bit store / load of a float pair.
-__device__ __forceinline__ void st_dev2(float2* p, float a, float b) {
-    const uint64_t v = static_cast<uint64_t>(__float_as_uint(a)) | (static_cast<uint64_t>(__float_as_uint(b)) << 32);
-    __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 ld_dev2(const float2* p) {
-    const uint64_t v =
-        __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return make_float2(__uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32)));
-}
-
-// Merge two (max, sum-of-exp2) softmax partials.
-__device__ __forceinline__ void merge_ml(float& m, float& l, float m2, float l2) {
-    if (m2 == -INFINITY) return;
-    if (m == -INFINITY) {
-        m = m2;
-        l = l2;
-        return;
-    }
-    const float mn = fmaxf(m, m2);
-    l = l * exp2f(m - mn) + l2 * exp2f(m2 - mn);
-    m = mn;
-}
-
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
     return static_cast<uint32_t>(vz::f32_to_bf16(a)) | (static_cast<uint32_t>(vz::f32_to_bf16(b)) << 16);
 }
 
-// XOR swizzles of the 16-byte chunks of a staged row in LDS (bank analysis in
-// the design notes).  K: row r of the tile.  V: row a of 4-row block b.
-__device__ __forceinline__ int kswz(int r) { return r & 15; }
-__device__ __forceinline__ int vswz(int a, int b) { return ((a << 1) + ((b & 1) << 3)) & 15; }
+// Half precision (round to nearest even) pack / unpack.
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+    const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
+    uint16_t ua, ub;
+    __builtin_memcpy(&ua, &ha, 2);
+    __builtin_memcpy(&ub, &hb, 2);
+    return static_cast<uint32_t>(ua) | (static_cast<uint32_t>(ub) << 16);
+}
+__device__ __forceinline__ float f16_to_f32(uint16_t x) {
+    _Float16 h;
+    __builtin_memcpy(&h, &x, 2);
+    return static_cast<float>(h);
+}
 
 template <int NW>
-__global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
+__global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
-    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache, float* __restrict__ score,
-    int32_t* __restrict__ pos, int32_t len, int32_t next_pos, float gamma, float scale_log2, int32_t Hq,
-    int32_t cap, int32_t n_chunks, int32_t nc_max, int32_t n_items, int32_t L, uint8_t* __restrict__ ws,
-    int32_t hdr_bytes) {
-    __shared__ uint32_t s_item;
-    __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][VT * D * 2];
-    __shared__ float s_psum[NW][CHUNK];
+    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache, int32_t* __restrict__ pos, int32_t len,
+    int32_t next_pos, float scale_log2, int32_t Hq, int32_t cap, int32_t n_chunks, int32_t nc_max, int32_t L,
+    uint8_t* __restrict__ ws, int32_t hdr_bytes) {
+    __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][TILE_BYTES];
 
     const int tid = threadIdx.x;
     // wave-uniform values go through readfirstlane so that addresses built
@@ -137,29 +148,20 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
     const int G = Hq / NW;
     const int g = w;                  // KV head of this wave
 
-    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
-    float2* part_ml = reinterpret_cast<float2*>(ws + hdr_bytes);
-    float* part_o = reinterpret_cast<float*>(ws + hdr_bytes) + 2 * L * nc_max * Hq;
-
-    if (tid == 0) s_item = atomicAdd(&hdr->ticket, 1u);
-    __syncthreads();
-    const int item = __builtin_amdgcn_readfirstlane(static_cast<int>(s_item));
-    if (item >= n_items) {  // the workspace was not zero-filled: flag it, touch nothing else
-        if (tid == 0) __hip_atomic_store(&hdr->error, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
-    }
-    const int l = item / n_chunks, c = item % n_chunks;
+    Partials part(ws, hdr_bytes, L, nc_max, Hq);
+    const int item = blockIdx.x;
+    const int l = item / n_chunks, c = item - (item / n_chunks) * n_chunks;
     const int T = len + 1;
-    const int k_begin = static_cast<int>(static_cast<int64_t>(c) * T / n_chunks);
-    const int k_end = static_cast<int>(static_cast<int64_t>(c + 1) * T / n_chunks);
-    const int nk = k_end - k_begin;
+    const int k_begin = chunk_begin(c, T, n_chunks);
+    const int nk = chunk_begin(c + 1, T, n_chunks) - k_begin;
     const size_t head_base = (static_cast<size_t>(l) * NW + g) * static_cast<size_t>(cap) * D;
     uint16_t* Kh = k_cache + head_base;
     uint16_t* Vh = v_cache + head_base;
 
     // Eq. (1) first: the chunk holding slot len writes the new row into the
-    // cache, so every key below is read from the cache the same way.
-    if (len >= k_begin && len < k_end) {
+    // cache (the wave of each KV head its own row, complete before its loads),
+    // so every key is read from the cache the same way.
+    if (len >= k_begin && len < k_begin + nk) {
         const uint16_t* kn = k_new + (l * NW + g) * D;
         const uint16_t* vn = v_new + (l * NW + g) * D;
         if (lane < 16)
@@ -170,7 +172,41 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
         if (tid == 0) pos[l * cap + len] = next_pos;
         __threadfence_block();
     }
-    __syncthreads();
+
+    // Staging: the chunk's K rows and then its V rows stream through the
+    // registers as one sequence of 8 tiles of 32 rows.  Instruction m of a
+    // tile reads rows 4m..4m+3 whole (lane = row 4m + q4, 16-byte column r16)
+    // with buffer loads from a descriptor based at the tile's first row and
+    // bounded to the chunk's rows, so rows past the chunk end read as zero and
+    // cost no memory traffic (their logits are masked, their probabilities
+    // are zero).  The descriptor is scalar; every load shares the lane offset.
+    const uint16_t* const kc = Kh + static_cast<size_t>(k_begin) * D;
+    const uint16_t* const vc = Vh + static_cast<size_t>(k_begin) * D;
+    const int lane_off = q4 * (D * 2) + 16 * r16;
+    uint4 stg[8];
+    auto load_tile = [&](const uint16_t* base, int u) {
+        const int rows = nk - VT * u > 0 ? nk - VT * u : 0;
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base) + VT * u * D, 0, rows * D * 2, kBufferDword3);
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lane_off + 4 * m * (D * 2), 0, 0);
+            __builtin_memcpy(&stg[m], &v, 16);
+        }
+    };
+    load_tile(kc, 0);
+
+    // Per-lane LDS bases.  Stores: lane (q4, r16) writes 16-byte column r16 of
+    // row 4m + q4 in instruction m.  K reads (A operand of S^T = K Q^T): row
+    // r16 (+16 for the odd tile), columns 4s + q4.  V reads (transposed B
+    // operand of P V): in each 16-lane group, row 4 q4 + r16 / 4 (+16 for
+    // keys 16..31 of the tile), 8 bytes at column 32 n + 16 ((r16 & 3) / 2) +
+    // 8 (r16 & 1).
+    uint8_t* const buf = s_tile[w];
+    uint8_t* const kw = buf + q4 * KSTRIDE + 16 * r16;
+    uint8_t* const vw = buf + q4 * VSTRIDE + 16 * r16;
+    const uint8_t* const kr = buf + r16 * KSTRIDE + 16 * q4;
+    const uint8_t* const vr = buf + (4 * q4 + (r16 >> 2)) * VSTRIDE + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
 
     // ---------------- pass 1: logits S^T = K Q^T ----------------
     uint4 qv[KSTEPS];  // B operand: Q^T, column r16 = query head (zero past G)
@@ -183,46 +219,23 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
             qv[s] = (r16 < G) ? v : make_uint4(0, 0, 0, 0);
         }
     }
-    uint8_t* buf = s_tile[w];
-    // Staging: instruction m of a 32-key tile reads rows 4m..4m+3 whole
-    // (lane = row 4m + q4, 16-byte chunk r16) with buffer loads addressed by
-    // 32-bit offsets from a descriptor bounded to the head's cap rows (reads
-    // outside it return zero).  Rows past the chunk end are clamped to its
-    // last row and masked out afterwards.
-    const int region = cap * D * 2;
-    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(Kh, 0, region, kBufferDword3);
-    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(Vh, 0, region, kBufferDword3);
-    uint4 stg[8];
-    auto load_tile = [&](const __amdgpu_buffer_rsrc_t& rs, int u) {
-#pragma unroll
-        for (int m = 0; m < 8; ++m) {
-            int j = k_begin + VT * u + 4 * m + q4;
-            j = j < k_end ? j : k_end - 1;
-            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, j * (D * 2) + 16 * r16, 0, 0);
-            __builtin_memcpy(&stg[m], &v, 16);
-        }
-    };
     // sp[u][i]: lanes with hi = 0 hold key 32u + 4 q4 + i, head hh; lanes with
     // hi = 1 hold key 32u + 16 + 4 q4 + i, head hh.
     float sp[PAIRS][4];
-    load_tile(krs, 0);
 #pragma unroll
     for (int u = 0; u < PAIRS; ++u) {
 #pragma unroll
-        for (int m = 0; m < 8; ++m) {
-            const int row = 4 * m + q4;
-            *reinterpret_cast<uint4*>(buf + 256 * row + 16 * (r16 ^ kswz(row))) = stg[m];
-        }
-        if (u + 1 < PAIRS) load_tile(krs, u + 1);
+        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(kw + 4 * KSTRIDE * m) = stg[m];
+        if (u + 1 < PAIRS) load_tile(kc, u + 1);
+        else load_tile(vc, 0);  // the first V tile follows the last K tile
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
         f32x4 acc[2];
 #pragma unroll
         for (int ti = 0; ti < 2; ++ti) {
-            const int row = 16 * ti + r16;
             acc[ti] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < KSTEPS; ++s) {
-                const uint4 a = *reinterpret_cast<const uint4*>(buf + 256 * row + 16 * ((4 * s + q4) ^ kswz(row)));
+                const uint4 a = *reinterpret_cast<const uint4*>(kr + 16 * KSTRIDE * ti + 64 * s);
                 acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qv[s]), acc[ti], 0, 0, 0);
             }
         }
@@ -236,7 +249,7 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
 
-    // ---------------- chunk statistics, published at once ----------------
+    // ---------------- chunk statistics ----------------
     // per head hh (8 lanes share it: q4 x hi); afterwards sp holds p~ = exp2(s - m_c)
     float m_c = -INFINITY;
 #pragma unroll
@@ -258,23 +271,23 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
     l_c += __shfl_xor(l_c, 32, 64);
     l_c += ror8(l_c);
     const int pbase = (l * nc_max + c) * Hq + g * G;  // < 2^31 (checked on the host)
-    if (q4 == 0 && r16 < G) st_dev2(&part_ml[pbase + r16], m_c, l_c);
-    load_tile(vrs, 0);
+    if (q4 == 0 && r16 < G) part.ml[pbase + r16] = make_float2(m_c, l_c);
 
-    // ---------------- pass 2: O = P V on the matrix cores ----------------
+    // ---------------- pass 2: O^T = V^T P^T on the matrix cores ----------------
+    // (D tile n: column = head r16, rows = channels 16 n + 4 q4 + 0..3, so each
+    // lane ends with runs of 4 channels of one head)
     f32x4 oacc[DTILES];
 #pragma unroll
     for (int n = 0; n < DTILES; ++n) oacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < PAIRS; ++u) {
 #pragma unroll
-        for (int m = 0; m < 8; ++m)
-            *reinterpret_cast<uint4*>(buf + 1024 * m + 256 * q4 + 16 * (r16 ^ vswz(q4, m))) = stg[m];
-        if (u + 1 < PAIRS) load_tile(vrs, u + 1);
-        // A operand P: row = head r16 (rows >= G feed output rows that are never
-        // stored), k-slots 8 q4 + i -> keys 32u + 4 q4 + i (i < 4) and
-        // 32u + 16 + 4 q4 + i - 4 (i >= 4): the even tile is in place, the odd
-        // tile comes back from the upper half of the row.
+        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vw + 4 * VSTRIDE * m) = stg[m];
+        if (u + 1 < PAIRS) load_tile(vc, u + 1);
+        // B operand P^T: column = head r16 (columns >= G feed output columns
+        // that are never stored), k-slots 8 q4 + i -> keys 32u + 4 q4 + i (i < 4)
+        // and 32u + 16 + 4 q4 + i - 4 (i >= 4): the even tile is in place, the
+        // odd tile comes back from the upper half of the row.
         float ev[4], od[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -289,138 +302,193 @@ __global__ __launch_bounds__(64 * NW, 2) void decode_attend_kernel(
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
 #pragma unroll
         for (int n = 0; n < DTILES; ++n) {
-            const int a = r16 >> 2;
-            const int cl = 2 * n + ((r16 & 3) >> 1);
-            const int half = (r16 & 1) * 8;
-            const uint8_t* pa0 = buf + 1024 * q4 + 256 * a + 16 * (cl ^ vswz(a, q4)) + half;
-            const uint8_t* pa1 = buf + 1024 * (4 + q4) + 256 * a + 16 * (cl ^ vswz(a, 4 + q4)) + half;
-            s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pa0));
-            s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pa1));
+            s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vr + 32 * n));
+            s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4*)(vr + 16 * VSTRIDE + 32 * n));
             uint4 bw;
             __builtin_memcpy(&bw.x, &b0, 8);
             __builtin_memcpy(&bw.z, &b1, 8);
-            oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, as_bf16x8(bw), oacc[n], 0, 0, 0);
+            oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(bw), pa, oacc[n], 0, 0, 0);
         }
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
-    // partial O (read by the combine kernel after this launch): plain stores
+    // ---------------- partial results: whole rows through LDS ----------------
+    // p~ (half) and O (bfloat16, relative to the chunk max) of the wave's G
+    // heads are staged in its free tile buffer, 256 bytes per head at a
+    // 320-byte stride, then written as 1 KB fully coalesced stores: the
+    // workspace holds both as rows of 256 bytes, heads of the wave adjacent.
     {
-        float* po = part_o + pbase * D;
+        constexpr int HS = 320;
+        uint8_t* const lp = buf;
+        uint8_t* const lo = buf + GMAX * HS;
+        if (hh < G) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int h = 4 * q4 + i;  // output row = query head of the group
-            if (h < G) {
-#pragma unroll
-                for (int n = 0; n < DTILES; ++n) po[h * D + 16 * n + r16] = oacc[n][i];
-            }
+            for (int u = 0; u < PAIRS; ++u)
+                *reinterpret_cast<uint2*>(lp + hh * HS + 2 * (VT * u + 16 * hi + 4 * q4)) =
+                    make_uint2(pack_f16x2(sp[u][0], sp[u][1]), pack_f16x2(sp[u][2], sp[u][3]));
         }
-    }
-
-    // ---------------- fold: A[j] = gamma A[j] + sum_h p_hj ----------------
-    // The chunk's old scores are loaded first, so their latency overlaps the
-    // wait for the statistics.
-    constexpr int KPT = (CHUNK + 64 * NW - 1) / (64 * NW);  // keys per thread
-    float* lsc = score + l * cap;
-    float a_old[KPT];
+        if (r16 < G) {
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-        const int k = tid + 64 * NW * i;
-        const int j = k_begin + k;
-        a_old[i] = (k < nk && j < len) ? lsc[j] : 0.f;
-    }
-    // Global (max, sum) of this wave's heads: lane (q4, hi, hh) polls head hh
-    // over chunks q4 + 4 hi + 8 k, 64 chunks per round, until no pair of the
-    // round is unpublished; the eight lanes of a head then merge.
-    float m_h = -INFINITY, l_h = 0.f;
-    {
-        const float2* hrow = part_ml + l * nc_max * Hq + g * G + (hh < G ? hh : 0);
-        const uint64_t t0 = wall_clock64();
-        for (int base = 0; base < n_chunks; base += 64) {
-            float2 v[8];
-            for (;;) {
-                bool ready = true;
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const int cc = base + q4 + 4 * hi + 8 * k;
-                    v[k] = cc < n_chunks ? ld_dev2(hrow + cc * Hq) : make_float2(-INFINITY, 1.f);
-                    ready = ready && v[k].y != 0.f;
-                }
-                if (__all(ready)) break;
-                if (wall_clock64() - t0 > kWaitTicks) {
-                    if (lane == 0) __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-#pragma unroll
-            for (int k = 0; k < 8; ++k) merge_ml(m_h, l_h, v[k].x, v[k].y);
+            for (int n = 0; n < DTILES; ++n)
+                *reinterpret_cast<uint2*>(lo + r16 * HS + 2 * (16 * n + 4 * q4)) =
+                    make_uint2(pack_bf16x2(oacc[n][0], oacc[n][1]), pack_bf16x2(oacc[n][2], oacc[n][3]));
         }
-        merge_ml(m_h, l_h, __shfl_xor(m_h, 16, 64), __shfl_xor(l_h, 16, 64));
-        merge_ml(m_h, l_h, __shfl_xor(m_h, 32, 64), __shfl_xor(l_h, 32, 64));
-        merge_ml(m_h, l_h, ror8(m_h), ror8(l_h));
-    }
-    const float fac = (hh < G) ? exp2f(m_c - m_h) / l_h : 0.f;  // p = p~ * fac
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): staged
+        uint8_t* const gp = reinterpret_cast<uint8_t*>(part.p) + static_cast<size_t>(pbase) * (CHUNK * 2);
+        uint8_t* const go = reinterpret_cast<uint8_t*>(part.o) + static_cast<size_t>(pbase) * (D * 2);
 #pragma unroll
-    for (int u = 0; u < PAIRS; ++u) {
-        if (VT * u < nk) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float pv = sp[u][i] * fac;
-                pv += __shfl_xor(pv, 1, 64);
-                pv += __shfl_xor(pv, 2, 64);
-                pv += __shfl_xor(pv, 4, 64);
-                if (hh == 0) s_psum[w][VT * u + 16 * hi + 4 * q4 + i] = pv;
+        for (int j = 0; j < GMAX * 256 / 1024; ++j) {
+            const int off = 1024 * j + 16 * lane;
+            if (off < G * 256) {
+                const int src = (off >> 8) * HS + (off & 255);
+                *reinterpret_cast<uint4*>(gp + off) = *reinterpret_cast<const uint4*>(lp + src);
+                *reinterpret_cast<uint4*>(go + off) = *reinterpret_cast<const uint4*>(lo + src);
             }
-        }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-        const int k = tid + 64 * NW * i;
-        if (k < nk) {
-            float a = 0.f;
-#pragma unroll
-            for (int gg = 0; gg < NW; ++gg) a += s_psum[gg][k];
-            lsc[k_begin + k] = gamma * a_old[i] + a;  // a_old = 0 for the new slot (zero pad of Eq. 6)
         }
     }
 }
 
-// Combine kernel: one workgroup of D threads per (layer, head):
-//   o_h = sum_c O_c,h exp2(m_c,h - m_h) / l_h over the layer's chunks.
-// It then zeroes the (max, sum) pairs it has read (and workgroup (0, 0) the
-// ticket): the attend kernel of the next call starts from a clean workspace.
-__global__ __launch_bounds__(D) void decode_combine_kernel(uint8_t* __restrict__ ws, uint16_t* __restrict__ out,
-                                                           int32_t Hq, int32_t n_chunks, int32_t nc_max, int32_t L,
-                                                           int32_t hdr_bytes) {
-    __shared__ float s_w[256];
-    __shared__ float s_m, s_l;
-    const int h = blockIdx.x, l = blockIdx.y, tid = threadIdx.x;
-    float2* ml = reinterpret_cast<float2*>(ws + hdr_bytes) + l * nc_max * Hq + h;
-    const float* po = reinterpret_cast<const float*>(ws + hdr_bytes) + 2 * L * nc_max * Hq + (l * nc_max * Hq + h) * D;
-    if (tid < 64) {  // wave 0: global (max, sum) of the head over the chunks
-        float m = -INFINITY, s = 0.f;
-        for (int cc = tid; cc < n_chunks; cc += 64) {
-            const float2 v = ml[cc * Hq];
-            merge_ml(m, s, v.x, v.y);
+// Output kernel, one workgroup of 256 threads per (head h, layer l).  Thread
+// t owns channels 8 (t % 16) .. +7 of the rows of chunks t / 16, t / 16 + 16,
+// ...: it merges them with a running max, o = sum_c O_c exp2(m_c - M) /
+// sum_c l_c exp2(m_c - M), and the 16 row groups then merge in LDS.  All
+// loads of a round (16-byte row pieces and the chunk pairs) are issued before
+// any use: indexes past the end are clamped and the values masked afterwards,
+// so no load sits behind a branch.  Also stores the layer's (max, 1 / sum) of
+// head h for the fold kernel.
+constexpr int OUT_THREADS = 256;
+constexpr int OUT_ROWS = OUT_THREADS / 16;  // row groups
+constexpr int OUT_BATCH = 8;                // chunks per row group and round
+__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(uint8_t* __restrict__ ws,
+                                                                   uint16_t* __restrict__ out, int32_t Hq,
+                                                                   int32_t n_chunks, int32_t nc_max, int32_t L,
+                                                                   int32_t hdr_bytes) {
+    __shared__ float s_acc[OUT_ROWS][D + 4];
+    __shared__ float s_m[OUT_ROWS], s_l[OUT_ROWS];
+    const int h = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    const int rg = t / 16, c8 = 8 * (t % 16);
+    Partials part(ws, hdr_bytes, L, nc_max, Hq);
+    const float2* ml = part.ml + static_cast<size_t>(l) * nc_max * Hq + h;
+    const uint16_t* po = part.o + (static_cast<size_t>(l) * nc_max * Hq + h) * D + c8;
+    float M = -INFINITY, S = 0.f, acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+    for (int c0 = rg; c0 < n_chunks; c0 += OUT_ROWS * OUT_BATCH) {
+        float2 st[OUT_BATCH];
+        uint4 xr[OUT_BATCH];
+#pragma unroll
+        for (int k = 0; k < OUT_BATCH; ++k) {
+            const int cc = min(c0 + OUT_ROWS * k, n_chunks - 1);
+            st[k] = ml[static_cast<size_t>(cc) * Hq];
+            xr[k] = *reinterpret_cast<const uint4*>(po + static_cast<size_t>(cc) * Hq * D);
         }
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) merge_ml(m, s, __shfl_xor(m, o, 64), __shfl_xor(s, o, 64));
-        if (tid == 0) {
-            s_m = m;
-            s_l = s;
+        for (int k = 0; k < OUT_BATCH; ++k) {
+            if (c0 + OUT_ROWS * k >= n_chunks) break;
+            if (st[k].x > M) {
+                const float r = exp2f(M - st[k].x);  // 0 while M is -inf
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc[i] *= r;
+                S *= r;
+                M = st[k].x;
+            }
+            const float wgt = exp2f(st[k].x - M);
+            float x[8];
+            vz::unpack16<VZ_BF16>(xr[k], x);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] += wgt * x[i];
+            S += wgt * st[k].y;
         }
     }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s_acc[rg][c8 + i] = acc[i];
+    if (t % 16 == 0) {
+        s_m[rg] = M;
+        s_l[rg] = S;
+    }
     __syncthreads();
-    const float m = s_m, inv_l = 1.0f / s_l;
-    for (int cc = tid; cc < n_chunks; cc += D) s_w[cc] = exp2f(ml[cc * Hq].x - m) * inv_l;
-    __syncthreads();
-    for (int cc = tid; cc < n_chunks; cc += D) ml[cc * Hq] = make_float2(0.f, 0.f);
-    if (h == 0 && l == 0 && tid == 0) reinterpret_cast<WsHeader*>(ws)->ticket = 0u;
+    if (t < D) {
+        float Mg = s_m[0];
+#pragma unroll
+        for (int r = 1; r < OUT_ROWS; ++r) Mg = fmaxf(Mg, s_m[r]);
+        float a = 0.f, sum = 0.f;
+#pragma unroll
+        for (int r = 0; r < OUT_ROWS; ++r) {
+            const float f = s_m[r] == -INFINITY ? 0.f : exp2f(s_m[r] - Mg);
+            a += s_acc[r][t] * f;
+            sum += s_l[r] * f;
+        }
+        const float il = 1.0f / sum;
+        out[(static_cast<size_t>(l) * Hq + h) * D + t] = vz::f32_to_bf16(a * il);
+        if (t == 0) part.layer[static_cast<size_t>(l) * Hq + h] = make_float2(Mg, il);
+    }
+}
+
+// Fold kernel, one workgroup of CHUNK threads per (chunk c, layer l), thread
+// = key: Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h with
+// f_h = exp2(m_c,h - M_h) / S_h (the new slot starts from 0).  Heads go in
+// rounds of 32: the round's p~ loads and factor loads are issued together
+// (p~ rows are complete, CHUNK entries each, so every load is in bounds;
+// heads past Hq are clamped and masked, so no load sits behind a branch).
+constexpr int FOLD_HEADS = 32;
+__global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const uint8_t* __restrict__ ws, float* __restrict__ score,
+                                                            int32_t len, float gamma, int32_t Hq, int32_t cap,
+                                                            int32_t n_chunks, int32_t nc_max, int32_t L,
+                                                            int32_t hdr_bytes) {
+    __shared__ float s_f[FOLD_HEADS];
+    const int c = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    const ConstPartials part(ws, hdr_bytes, L, nc_max, Hq);
+    const int T = len + 1;
+    const int k_begin = chunk_begin(c, T, n_chunks);
+    const int nk = chunk_begin(c + 1, T, n_chunks) - k_begin;
+    const int j = k_begin + (t < nk ? t : 0);
+    float* a = score + static_cast<size_t>(l) * cap + j;
+    const float a_ld = *a;
+    const float a_old = (t < nk && j < len) ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
+    const size_t cbase = (static_cast<size_t>(l) * nc_max + c) * Hq;
+    const uint16_t* pp = part.p + cbase * CHUNK + t;
     float acc = 0.f;
-#pragma unroll 8
-    for (int cc = 0; cc < n_chunks; ++cc) acc += s_w[cc] * po[cc * Hq * D + tid];
-    out[(l * Hq + h) * D + tid] = vz::f32_to_bf16(acc);
+    for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
+        uint16_t pr[FOLD_HEADS];
+#pragma unroll
+        for (int k = 0; k < FOLD_HEADS; ++k) pr[k] = pp[min(hb + k, Hq - 1) * CHUNK];
+        if (t < FOLD_HEADS && hb + t < Hq) {
+            const float2 gl = part.layer[static_cast<size_t>(l) * Hq + hb + t];
+            s_f[t] = exp2f(part.ml[cbase + hb + t].x - gl.x) * gl.y;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < FOLD_HEADS; ++k)
+            if (hb + k < Hq) acc += f16_to_f32(pr[k]) * s_f[k];
+        __syncthreads();
+    }
+    if (t < nk) *a = gamma * a_old + acc;
+}
+
+int32_t fused_chunks(int32_t T) { return (T + CHUNK - 1) / CHUNK; }
+
+template <int NW>
+hipError_t launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
+    const int T = a.len + 1;
+    const int n_chunks = fused_chunks(T);
+    const int nc_max = fused_chunks(a.cap);
+    const float scale = (a.sm_scale > 0.f ? a.sm_scale : 1.0f / sqrtf(static_cast<float>(D))) * kLog2e;
+    const int hdr = static_cast<int>(vz_decode_hdr_bytes(a.L));
+    auto* ws = static_cast<uint8_t*>(a.ws);
+    hipLaunchKernelGGL((decode_attend_kernel<NW>), dim3(a.L * n_chunks), dim3(64 * NW), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_new),
+                       static_cast<const uint16_t*>(a.v_new), static_cast<uint16_t*>(a.k_cache),
+                       static_cast<uint16_t*>(a.v_cache), a.pos, a.len, a.next_pos, scale, a.Hq, a.cap, n_chunks,
+                       nc_max, a.L, ws, hdr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(decode_output_kernel, dim3(a.Hq, a.L), dim3(OUT_THREADS), 0, stream, ws,
+                       static_cast<uint16_t*>(a.out), a.Hq, n_chunks, nc_max, a.L, hdr);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(decode_fold_kernel, dim3(n_chunks, a.L), dim3(CHUNK), 0, stream, ws, a.score, a.len, a.gamma,
+                       a.Hq, a.cap, n_chunks, nc_max, a.L, hdr);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -428,55 +496,34 @@ __global__ __launch_bounds__(D) void decode_combine_kernel(uint8_t* __restrict__
 // ---- sizing shared with the host API ----
 size_t vz_decode_hdr_bytes(int32_t L) {
     (void)L;
-    return sizeof(WsHeader);
+    return kHeaderBytes;
 }
-
-int32_t vz_decode_fused_chunks(int32_t T) { return (T + CHUNK - 1) / CHUNK; }
 
 bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap, int32_t L) {
     if (dtype != VZ_BF16 || d != D) return false;
     if (!(Hkv == 1 || Hkv == 2 || Hkv == 4 || Hkv == 8)) return false;
     if (Hq % Hkv != 0 || Hq / Hkv > GMAX) return false;
-    // 32-bit element offsets inside the kernels: partials, scores, positions,
-    // outputs, one head's rows
-    const int64_t ncm = vz_decode_fused_chunks(cap);
-    if (static_cast<int64_t>(L) * ncm * Hq * (D + 2) >= (int64_t(1) << 31)) return false;
+    const int64_t ncm = fused_chunks(cap);
+    if (ncm > MAX_CHUNKS) return false;
+    // 32-bit offsets inside the kernels: partials, scores, positions, outputs,
+    // one head's rows, chunk bounds
+    if (static_cast<int64_t>(L) * ncm * Hq * CHUNK >= (int64_t(1) << 31)) return false;
     if (static_cast<int64_t>(L) * cap >= (int64_t(1) << 31)) return false;
     if (static_cast<int64_t>(cap) * D * 2 >= (int64_t(1) << 31)) return false;
     if (static_cast<int64_t>(L) * Hq * D >= (int64_t(1) << 31)) return false;
-    return ncm <= 256;  // chunks of one layer must fit on the GPU at once
+    return static_cast<int64_t>(cap) < (int64_t(1) << 22);
 }
 
 size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int32_t cap) {
-    const size_t ncm = static_cast<size_t>(vz_decode_fused_chunks(cap));
-    return vz_decode_hdr_bytes(L) + static_cast<size_t>(L) * ncm * Hq * (sizeof(float2) + sizeof(float) * D);
+    return vz_decode_hdr_bytes(L) + partials_bytes(L, fused_chunks(cap), Hq);
 }
 
 hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
-    const int T = a.len + 1;
-    const int n_chunks = vz_decode_fused_chunks(T);
-    const int nc_max = vz_decode_fused_chunks(a.cap);
-    const int n_items = a.L * n_chunks;
-    const float scale = (a.sm_scale > 0.f ? a.sm_scale : 1.0f / sqrtf(static_cast<float>(D))) * kLog2e;
-    const int hdr = static_cast<int>(vz_decode_hdr_bytes(a.L));
-    auto* ws = static_cast<uint8_t*>(a.ws);
-#define VZ_LAUNCH_ATTEND(NW)                                                                                     \
-    hipLaunchKernelGGL((decode_attend_kernel<NW>), dim3(n_items), dim3(64 * NW), 0, stream,                     \
-                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_new),                \
-                       static_cast<const uint16_t*>(a.v_new), static_cast<uint16_t*>(a.k_cache),                \
-                       static_cast<uint16_t*>(a.v_cache), a.score, a.pos, a.len, a.next_pos, a.gamma, scale,    \
-                       a.Hq, a.cap, n_chunks, nc_max, n_items, a.L, ws, hdr)
     switch (a.Hkv) {
-        case 1: VZ_LAUNCH_ATTEND(1); break;
-        case 2: VZ_LAUNCH_ATTEND(2); break;
-        case 4: VZ_LAUNCH_ATTEND(4); break;
-        case 8: VZ_LAUNCH_ATTEND(8); break;
+        case 1: return launch_decode_fused<1>(a, stream);
+        case 2: return launch_decode_fused<2>(a, stream);
+        case 4: return launch_decode_fused<4>(a, stream);
+        case 8: return launch_decode_fused<8>(a, stream);
         default: return hipErrorInvalidValue;
     }
-#undef VZ_LAUNCH_ATTEND
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_combine_kernel, dim3(a.Hq, a.L), dim3(D), 0, stream, ws,
-                       static_cast<uint16_t*>(a.out), a.Hq, n_chunks, nc_max, a.L, hdr);
-    return hipGetLastError();
 }

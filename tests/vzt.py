@@ -112,16 +112,11 @@ class GpuCache:
         return self.dtype == synth.DT_BF16 and self.d == 128 and self.Hkv in (1, 2, 4, 8) and G <= 8
 
     def check_decode_workspace(self):
-        """After every call the decode workspace header (ticket, error flag) is
-        zero again, and on the MFMA path so are the per-chunk softmax pairs."""
+        """After every call the decode workspace header is still zero (no
+        kernel flagged an error in it)."""
         torch().cuda.synchronize()
         hdr = from_dev(self.ws_dec[:256]).view(np.uint32)
-        assert hdr[1] == 0, "decode kernel flagged an error (expired wait or unzeroed workspace)"
-        assert not hdr.any(), f"decode workspace header not cleared: {hdr[:4]}"
-        if self.fused_decode_path():
-            ncm = (self.cap + 255) // 256
-            ml = from_dev(self.ws_dec[256: 256 + 8 * self.L * ncm * self.Hq]).view(np.uint32)
-            assert not ml.any(), "softmax pairs not cleared after the call"
+        assert not hdr.any(), f"decode workspace header not zero: {hdr[:4]}"
 
     def evict(self, budget, n_sink=4, n_recent=-1, kept=None):
         self.len = self.vz.voxzip_evict_compact(self.k, self.v, self.score, self.pos, self.len, budget,
