@@ -131,10 +131,9 @@ VZ_API int voxzip_fuse_spans(const void *k_in, const void *v_in, int32_t T_in,
  *  gamma        decay in [0, 1] (1 = plain accumulation).
  *  sm_scale     softmax scale; <= 0 selects 1 / sqrt(d).
  *  workspace    device scratch of at least voxzip_workspace_bytes(VZ_OP_DECODE,
- *               ...) bytes.  It must be zero-filled once after allocation;
- *               every call leaves the parts that must start at zero zeroed
- *               again, so later calls need no clearing.  One workspace must
- *               not be used by two calls that can run at the same time.
+ *               ...) bytes (per-chunk partial results); it needs no
+ *               initialisation.  One workspace must not be used by two calls
+ *               that can run at the same time.
  * The caller advances len and next_pos by one after the call.
  * Errors: VZ_ERR_INVALID (null pointer, gamma outside [0,1], len < 0),
  * VZ_ERR_CAPACITY (len + 1 > cap), VZ_ERR_SHAPE, VZ_ERR_UNSUPPORTED,
@@ -184,6 +183,119 @@ VZ_API int voxzip_evict_compact(void *k_cache, void *v_cache, float *score, int3
  */
 VZ_API size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_heads,
                               int32_t kv_heads, int32_t d, int32_t cap);
+
+/*
+ * Ragged batches
+ * --------------
+ * The *_ragged entry points serve n_seqs independent sequences (each with its
+ * own length, capacity, budget and positions) in one launch sequence, so a
+ * batch of sequences costs one call per step instead of one per sequence.
+ * Every operation is the one of the single-sequence entry point, applied to
+ * each sequence on its own (Sec. 3.2.1 per request, Sec. 3.1 and 3.2.2 per
+ * decode step).
+ *
+ *  Packed layout: one cache [n_layers][kv_heads][total][d] (scores and
+ *  positions [n_layers][total]); sequence s owns slots seq_base[s] ..
+ *  seq_base[s] + cap[s] - 1 of every plane, and its slot j is the single-call
+ *  slot j.  Sequences must not overlap.  total <= 2^26, 1 <= n_seqs <= 32768.
+ *  Per-sequence values (seq_base int64, cap / len / budget / next_pos int32,
+ *  [n_seqs] each) are DEVICE arrays, read by the kernels: host code never
+ *  waits for them, so a whole serving loop can stay on the device.
+ *  status: NULL or int32 [n_seqs], device: receives VZ_OK per served
+ *  sequence, or the error code of a sequence whose values are out of range;
+ *  such a sequence is skipped (nothing of it is read or written, its outputs
+ *  keep their previous contents).  Host-side errors are returned as usual.
+ *
+ * Workspace bytes of a ragged call (0 on a bad op or sizes out of range).
+ */
+VZ_API size_t voxzip_workspace_bytes_ragged(int32_t op, int32_t n_layers, int32_t n_q_heads,
+                                            int32_t kv_heads, int32_t d, int64_t total,
+                                            int32_t n_seqs);
+
+/*
+ * Ragged twin of voxzip_fuse_spans (Sec. 3.2.1, Eq. 4-5).
+ *  k_in, v_in   [n_layers][kv_heads][total_in][d]; sequence s reads input rows
+ *               in_base[s] .. in_base[s] + T_in[s] - 1 (int64 / int32 [n_seqs]).
+ *  span_off     int32 [total_off]; sequence s's offsets are
+ *               span_off[off_base[s] .. off_base[s] + n_spans[s]] (int64 /
+ *               int32 [n_seqs]), relative to its first input row, with the
+ *               rules of voxzip_fuse_spans.
+ *  max_spans    host bound on every n_spans[s] (sizes the grid); a sequence
+ *               with more spans gets VZ_ERR_CAPACITY.
+ *  anchor_k/v   NULL, or laid out like the outputs (row j of sequence s at
+ *               slot seq_base[s] + j).
+ *  k_out, v_out, score_out, pos_out  packed outputs; sequence s gets
+ *               n_spans[s] rows from slot seq_base[s] (n_spans[s] <= cap[s]),
+ *               pos = 0 .. n_spans[s] - 1, score 0.
+ * Per-sequence errors (status): VZ_ERR_INVALID (a range outside its array),
+ * VZ_ERR_SHAPE (n_spans > T_in), VZ_ERR_CAPACITY (n_spans > cap or > max_spans).
+ * Returned errors: VZ_ERR_INVALID (null pointer, aliasing), VZ_ERR_SHAPE,
+ * VZ_ERR_UNSUPPORTED.
+ */
+VZ_API int voxzip_fuse_spans_ragged(const void *k_in, const void *v_in, const int64_t *in_base,
+                                    const int32_t *T_in, int64_t total_in, const int32_t *span_off,
+                                    const int64_t *off_base, const int32_t *n_spans,
+                                    int64_t total_off, int32_t max_spans, const void *anchor_k,
+                                    const void *anchor_v, void *k_out, void *v_out, float *score_out,
+                                    int32_t *pos_out, const int64_t *seq_base, const int32_t *cap,
+                                    int64_t total, int32_t n_seqs, int32_t *status,
+                                    int32_t n_layers, int32_t kv_heads, int32_t d, int32_t dtype,
+                                    void *stream);
+
+/*
+ * Ragged twin of voxzip_decode_attend_score (Sec. 3.1 Eq. 1-2, Sec. 3.2.2
+ * Eq. 6): every sequence s appends its token at slot len[s] with position
+ * next_pos[s], attends over its len[s] + 1 slots and folds its scores.
+ *  q, out       [n_seqs][n_layers][n_q_heads][d];
+ *  k_new, v_new [n_seqs][n_layers][kv_heads][d].
+ *  len, next_pos, cap, seq_base   device [n_seqs] (len and next_pos are not
+ *               modified: the caller advances them, e.g. with one add).
+ *  workspace    at least voxzip_workspace_bytes_ragged(VZ_OP_DECODE, ...)
+ *               bytes; no initialisation needed; one call at a time per
+ *               workspace.
+ * Each sequence's results are bit-identical to a single-sequence call on
+ * the same data.
+ * Per-sequence errors (status): VZ_ERR_INVALID (negative len or next_pos, a
+ * range outside the planes), VZ_ERR_CAPACITY (len + 1 > cap, or sequences that
+ * overlap so that their chunks exceed the planes).
+ * Returned errors: as voxzip_decode_attend_score, plus VZ_ERR_SHAPE for
+ * n_seqs or total out of range.
+ */
+VZ_API int voxzip_decode_attend_score_ragged(const void *q, const void *k_new, const void *v_new,
+                                             void *k_cache, void *v_cache, float *score,
+                                             int32_t *pos, void *out, const int64_t *seq_base,
+                                             const int32_t *cap, const int32_t *len,
+                                             const int32_t *next_pos, int64_t total,
+                                             int32_t n_seqs, float gamma, float sm_scale,
+                                             int32_t n_layers, int32_t n_q_heads, int32_t kv_heads,
+                                             int32_t d, int32_t dtype, int32_t *status,
+                                             void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Ragged twin of voxzip_evict_compact (Sec. 3.2.2, Eq. 7-9): each sequence
+ * with len[s] > budget[s] keeps its sinks (pos < n_sink), its recent window
+ * (pos >= next_pos[s] - M, M = n_recent, or budget[s] / 5 when n_recent < 0)
+ * and the top middle slots by score, compacted into its slots 0 ..
+ * budget[s] - 1.
+ *  kept_pos_out NULL, or int32 [n_layers][total]: sequence s's kept positions,
+ *               ascending, from slot seq_base[s] (needs next_pos[s] <= 2^18).
+ *  new_len_out  NULL, or device int32 [n_seqs]: min(len, budget) per served
+ *               sequence (len for a skipped one); must not overlap len.
+ *  workspace    at least voxzip_workspace_bytes_ragged(VZ_OP_EVICT, ...) bytes.
+ * Per-sequence errors (status): VZ_ERR_INVALID (a range outside the planes,
+ * budget < 1, n_sink + M > budget, next_pos < len), VZ_ERR_CAPACITY
+ * (len > cap), VZ_ERR_UNSUPPORTED (kept_pos_out with next_pos > 2^18).
+ * Returned errors: VZ_ERR_INVALID (null pointer, n_sink < 0, new_len_out
+ * overlapping len), VZ_ERR_SHAPE, VZ_ERR_UNSUPPORTED, VZ_ERR_WORKSPACE.
+ */
+VZ_API int voxzip_evict_compact_ragged(void *k_cache, void *v_cache, float *score, int32_t *pos,
+                                       const int64_t *seq_base, const int32_t *cap,
+                                       const int32_t *len, const int32_t *budget,
+                                       const int32_t *next_pos, int64_t total, int32_t n_seqs,
+                                       int32_t n_sink, int32_t n_recent, int32_t *kept_pos_out,
+                                       int32_t *new_len_out, int32_t *status, int32_t n_layers,
+                                       int32_t kv_heads, int32_t d, int32_t dtype, void *workspace,
+                                       size_t ws_bytes, void *stream);
 
 /* Text of a status code (static storage). */
 VZ_API const char *voxzip_status_string(int status);

@@ -47,7 +47,17 @@ def lib() -> ctypes.CDLL:
     L.voxzip_build_span_offsets.restype = ctypes.c_int
     L.voxzip_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
     L.voxzip_workspace_bytes.restype = sz
-    for f in (L.voxzip_fuse_spans, L.voxzip_decode_attend_score, L.voxzip_evict_compact):
+    i64 = ctypes.c_int64
+    L.voxzip_workspace_bytes_ragged.argtypes = [i32, i32, i32, i32, i32, i64, i32]
+    L.voxzip_workspace_bytes_ragged.restype = sz
+    L.voxzip_fuse_spans_ragged.argtypes = [P, P, P, P, i64, P, P, P, i64, i32, P, P, P, P, P, P, P, P, i64, i32,
+                                           P, i32, i32, i32, i32, P]
+    L.voxzip_decode_attend_score_ragged.argtypes = [P, P, P, P, P, P, P, P, P, P, P, P, i64, i32, f32, f32,
+                                                    i32, i32, i32, i32, i32, P, P, sz, P]
+    L.voxzip_evict_compact_ragged.argtypes = [P, P, P, P, P, P, P, P, P, i64, i32, i32, i32, P, P, P,
+                                              i32, i32, i32, i32, P, sz, P]
+    for f in (L.voxzip_fuse_spans, L.voxzip_decode_attend_score, L.voxzip_evict_compact,
+              L.voxzip_fuse_spans_ragged, L.voxzip_decode_attend_score_ragged, L.voxzip_evict_compact_ragged):
         f.restype = ctypes.c_int
     L.voxzip_status_string.argtypes = [ctypes.c_int]
     L.voxzip_status_string.restype = ctypes.c_char_p
@@ -157,3 +167,83 @@ def workspace(op: int, n_layers: int, n_q_heads: int, kv_heads: int, d: int, cap
     import torch
     n = voxzip_workspace_bytes(op, n_layers, n_q_heads, kv_heads, d, cap)
     return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
+
+
+# ---- ragged batches: packed caches [L][H][total][d], per-sequence device arrays ----
+
+def _seq_array(t, n: int, dtype_name: str, what: str):
+    """Device pointer of a per-sequence array (int32 or int64, n entries)."""
+    import torch
+    want = torch.int64 if dtype_name == "int64" else torch.int32
+    if t.dtype != want:
+        raise TypeError(f"{what} must be {dtype_name}")
+    if t.numel() != n:
+        raise ValueError(f"{what} must have one entry per sequence ({n})")
+    return _ptr(t)
+
+
+def voxzip_workspace_bytes_ragged(op: int, n_layers: int, n_q_heads: int, kv_heads: int, d: int, total: int,
+                                  n_seqs: int) -> int:
+    return int(lib().voxzip_workspace_bytes_ragged(op, n_layers, n_q_heads, kv_heads, d, int(total), n_seqs))
+
+
+def workspace_ragged(op: int, n_layers: int, n_q_heads: int, kv_heads: int, d: int, total: int, n_seqs: int,
+                     device="cuda"):
+    """A zero-filled workspace tensor for a ragged call."""
+    import torch
+    n = voxzip_workspace_bytes_ragged(op, n_layers, n_q_heads, kv_heads, d, total, n_seqs)
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=device)
+
+
+def voxzip_fuse_spans_ragged(k_in, v_in, in_base, T_in, span_off, off_base, n_spans, max_spans: int,
+                             k_out, v_out, score_out, pos_out, seq_base, cap, status=None,
+                             anchor_k=None, anchor_v=None, stream=None) -> None:
+    """Stage-1 fusion of every sequence of a ragged batch; k_in/v_in
+    [L][H][total_in][d], span_off int32 [total_off], outputs [L][H][total][d]."""
+    L, H, total_in, d = k_in.shape
+    total = k_out.shape[2]
+    n = seq_base.numel()
+    _check(lib().voxzip_fuse_spans_ragged(
+        _ptr(k_in), _ptr(v_in), _seq_array(in_base, n, "int64", "in_base"), _seq_array(T_in, n, "int32", "T_in"),
+        total_in, _ptr(span_off), _seq_array(off_base, n, "int64", "off_base"),
+        _seq_array(n_spans, n, "int32", "n_spans"), span_off.numel(), int(max_spans), _ptr(anchor_k),
+        _ptr(anchor_v), _ptr(k_out), _ptr(v_out), _ptr(score_out), _ptr(pos_out),
+        _seq_array(seq_base, n, "int64", "seq_base"), _seq_array(cap, n, "int32", "cap"), total, n,
+        None if status is None else _seq_array(status, n, "int32", "status"), L, H, d, _dtype_code(k_in),
+        _stream(stream)))
+
+
+def voxzip_decode_attend_score_ragged(q, k_new, v_new, k_cache, v_cache, score, pos, out, seq_base, cap, length,
+                                      next_pos, gamma, sm_scale=0.0, status=None, workspace=None,
+                                      stream=None) -> None:
+    """One decode step of every sequence of a ragged batch; q/out [S][L][Hq][d],
+    k_new/v_new [S][L][Hkv][d], caches [L][Hkv][total][d]; length and next_pos
+    int32 [S] on the device (not advanced here)."""
+    L, Hkv, total, d = k_cache.shape
+    n, Hq = q.shape[0], q.shape[2]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().voxzip_decode_attend_score_ragged(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(score), _ptr(pos), _ptr(out),
+        _seq_array(seq_base, n, "int64", "seq_base"), _seq_array(cap, n, "int32", "cap"),
+        _seq_array(length, n, "int32", "length"), _seq_array(next_pos, n, "int32", "next_pos"), total, n,
+        float(gamma), float(sm_scale), L, Hq, Hkv, d, _dtype_code(k_cache),
+        None if status is None else _seq_array(status, n, "int32", "status"), _ptr(workspace), ws_bytes,
+        _stream(stream)))
+
+
+def voxzip_evict_compact_ragged(k_cache, v_cache, score, pos, seq_base, cap, length, budget, next_pos,
+                                n_sink=4, n_recent=-1, kept_pos_out=None, new_len_out=None, status=None,
+                                workspace=None, stream=None) -> None:
+    """Stage-2 eviction of every sequence of a ragged batch, in place;
+    new_len_out (int32 [S], device) receives min(length, budget)."""
+    L, Hkv, total, d = k_cache.shape
+    n = seq_base.numel()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().voxzip_evict_compact_ragged(
+        _ptr(k_cache), _ptr(v_cache), _ptr(score), _ptr(pos), _seq_array(seq_base, n, "int64", "seq_base"),
+        _seq_array(cap, n, "int32", "cap"), _seq_array(length, n, "int32", "length"),
+        _seq_array(budget, n, "int32", "budget"), _seq_array(next_pos, n, "int32", "next_pos"), total, n,
+        int(n_sink), int(n_recent), _ptr(kept_pos_out),
+        None if new_len_out is None else _seq_array(new_len_out, n, "int32", "new_len_out"),
+        None if status is None else _seq_array(status, n, "int32", "status"), L, Hkv, d, _dtype_code(k_cache),
+        _ptr(workspace), ws_bytes, _stream(stream)))

@@ -34,6 +34,15 @@ int check_common(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtyp
     if (L < 1 || Hkv < 1 || d < 1) return fail(VZ_ERR_SHAPE, fn, "sizes must be positive");
     if (dtype != VZ_F32 && dtype != VZ_BF16) return fail(VZ_ERR_UNSUPPORTED, fn, "dtype must be VZ_F32 or VZ_BF16");
     if (d != 64 && d != 128) return fail(VZ_ERR_UNSUPPORTED, fn, "head size must be 64 or 128");
+    if (L > 65535) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 65535 layers");
+    return VZ_OK;
+}
+
+int check_ragged(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtype, int64_t total, int32_t n_seqs) {
+    int rc = check_common(fn, L, Hkv, d, dtype);
+    if (rc) return rc;
+    if (n_seqs < 1 || n_seqs > kRaggedMaxSeqs) return fail(VZ_ERR_SHAPE, fn, "n_seqs must be in [1, 32768]");
+    if (total < 1 || total > kRaggedMaxTotal) return fail(VZ_ERR_SHAPE, fn, "total must be in [1, 2^26]");
     return VZ_OK;
 }
 
@@ -63,9 +72,21 @@ size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_heads, i
     if (n_layers < 1 || kv_heads < 1 || d < 1 || cap < 1) return 0;
     if (op == VZ_OP_DECODE) {
         if (n_q_heads < 1) return 0;
-        return vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap);
+        return vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap, 0);
     }
-    if (op == VZ_OP_EVICT) return vz_evict_ws_bytes(n_layers, kv_heads, d, cap);
+    if (op == VZ_OP_EVICT) return vz_evict_ws_bytes(n_layers, cap, 0);
+    return 0;
+}
+
+size_t voxzip_workspace_bytes_ragged(int32_t op, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
+                                     int64_t total, int32_t n_seqs) {
+    if (n_layers < 1 || kv_heads < 1 || d < 1 || total < 1 || total > kRaggedMaxTotal) return 0;
+    if (n_seqs < 1 || n_seqs > kRaggedMaxSeqs) return 0;
+    if (op == VZ_OP_DECODE) {
+        if (n_q_heads < 1) return 0;
+        return vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, total, n_seqs);
+    }
+    if (op == VZ_OP_EVICT) return vz_evict_ws_bytes(n_layers, total, n_seqs);
     return 0;
 }
 
@@ -130,10 +151,10 @@ int voxzip_decode_attend_score(const void* q, const void* k_new, const void* v_n
     if (cap < 1 || len + 1 > cap) return fail(VZ_ERR_CAPACITY, fn, "no free slot for the new token");
     if (!(gamma >= 0.f && gamma <= 1.f)) return fail(VZ_ERR_INVALID, fn, "gamma must be in [0, 1]");
     if (!isfinite(sm_scale)) return fail(VZ_ERR_INVALID, fn, "sm_scale must be finite");
-    const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap);
+    const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap, 0);
     if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
     VzDecodeArgs a{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
-                   n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, ws_bytes};
+                   n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, ws_bytes, VzRagged{}};
     hipError_t e = vz_launch_decode(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
 }
@@ -157,28 +178,118 @@ int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* po
         return fail(VZ_ERR_UNSUPPORTED, fn, "kept_pos_out needs next_pos <= 262144");
     const bool work = len > budget || kept_pos_out != nullptr;
     if (work) {
-        const size_t need = vz_evict_ws_bytes(n_layers, kv_heads, d, cap);
+        const size_t need = vz_evict_ws_bytes(n_layers, cap, 0);
         if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
     }
     *new_len_out = len < budget ? len : budget;
     if (!work) return VZ_OK;
     VzEvictArgs a{k_cache, v_cache, score, pos, len, budget, n_sink, M, next_pos, kept_pos_out,
-                  n_layers, kv_heads, d, cap, dtype, workspace, ws_bytes};
+                  n_layers, kv_heads, d, cap, dtype, workspace, ws_bytes, VzRagged{}, nullptr};
+    hipError_t e = vz_launch_evict(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+int voxzip_fuse_spans_ragged(const void* k_in, const void* v_in, const int64_t* in_base, const int32_t* T_in,
+                             int64_t total_in, const int32_t* span_off, const int64_t* off_base,
+                             const int32_t* n_spans, int64_t total_off, int32_t max_spans, const void* anchor_k,
+                             const void* anchor_v, void* k_out, void* v_out, float* score_out, int32_t* pos_out,
+                             const int64_t* seq_base, const int32_t* cap, int64_t total, int32_t n_seqs,
+                             int32_t* status, int32_t n_layers, int32_t kv_heads, int32_t d, int32_t dtype,
+                             void* stream) {
+    static const char* fn = "voxzip_fuse_spans_ragged";
+    if (!k_in || !v_in || !in_base || !T_in || !span_off || !off_base || !n_spans || !k_out || !v_out ||
+        !score_out || !pos_out || !seq_base || !cap)
+        return fail(VZ_ERR_INVALID, fn, "null pointer");
+    if ((anchor_k == nullptr) != (anchor_v == nullptr))
+        return fail(VZ_ERR_INVALID, fn, "anchor_k and anchor_v must both be given or both be NULL");
+    int rc = check_ragged(fn, n_layers, kv_heads, d, dtype, total, n_seqs);
+    if (rc) return rc;
+    if (total_in < 0 || total_off < 1 || max_spans < 0) return fail(VZ_ERR_SHAPE, fn, "negative size");
+    if (total_in > kRaggedMaxTotal || max_spans > total) return fail(VZ_ERR_SHAPE, fn, "size out of range");
+    if (2 * static_cast<int64_t>(kv_heads) > 65535) return fail(VZ_ERR_UNSUPPORTED, fn, "too many KV heads");
+    if ((static_cast<int64_t>(max_spans) + 15) / 16 * n_seqs >= (int64_t(1) << 31))
+        return fail(VZ_ERR_UNSUPPORTED, fn, "max_spans x n_seqs too large");
+    const size_t es = elem_size(dtype);
+    const size_t in_bytes = static_cast<size_t>(n_layers) * kv_heads * total_in * d * es;
+    const size_t out_bytes = static_cast<size_t>(n_layers) * kv_heads * total * d * es;
+    const void* ins[2] = {k_in, v_in};
+    void* outs[2] = {k_out, v_out};
+    for (const void* i : ins)
+        for (void* o : outs)
+            if (in_bytes && overlaps(i, in_bytes, o, out_bytes))
+                return fail(VZ_ERR_INVALID, fn, "an input aliases an output");
+    if (overlaps(k_out, out_bytes, v_out, out_bytes)) return fail(VZ_ERR_INVALID, fn, "k_out and v_out overlap");
+    VzFuseRaggedArgs a{k_in,     v_in,     in_base,  T_in,     span_off, off_base,  n_spans,  anchor_k,
+                       anchor_v, k_out,    v_out,    score_out, pos_out, seq_base,  cap,      status,
+                       n_seqs,   total_in, total_off, total,   max_spans, n_layers, kv_heads, d,
+                       dtype};
+    hipError_t e = vz_launch_fuse_ragged(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+int voxzip_decode_attend_score_ragged(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                                      void* v_cache, float* score, int32_t* pos, void* out, const int64_t* seq_base,
+                                      const int32_t* cap, const int32_t* len, const int32_t* next_pos, int64_t total,
+                                      int32_t n_seqs, float gamma, float sm_scale, int32_t n_layers,
+                                      int32_t n_q_heads, int32_t kv_heads, int32_t d, int32_t dtype,
+                                      int32_t* status, void* workspace, size_t ws_bytes, void* stream) {
+    static const char* fn = "voxzip_decode_attend_score_ragged";
+    if (!q || !k_new || !v_new || !k_cache || !v_cache || !score || !pos || !out || !seq_base || !cap || !len ||
+        !next_pos)
+        return fail(VZ_ERR_INVALID, fn, "null pointer");
+    int rc = check_ragged(fn, n_layers, kv_heads, d, dtype, total, n_seqs);
+    if (rc) return rc;
+    if (n_q_heads < 1 || n_q_heads % kv_heads != 0)
+        return fail(VZ_ERR_SHAPE, fn, "n_q_heads must be a positive multiple of kv_heads");
+    if (n_q_heads / kv_heads > 16) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 16 query heads per KV head");
+    if (n_q_heads > 256) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 256 query heads");
+    if (!(gamma >= 0.f && gamma <= 1.f)) return fail(VZ_ERR_INVALID, fn, "gamma must be in [0, 1]");
+    if (!isfinite(sm_scale)) return fail(VZ_ERR_INVALID, fn, "sm_scale must be finite");
+    const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, total, n_seqs);
+    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    VzRagged rg{seq_base, cap, len, next_pos, nullptr, status, n_seqs, total};
+    VzDecodeArgs a{q,  k_new, v_new, k_cache, v_cache, score, pos,   out,       0,        0,  gamma, sm_scale,
+                   n_layers, n_q_heads, kv_heads, d, 0, dtype, workspace, ws_bytes, rg};
+    hipError_t e = vz_launch_decode(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+int voxzip_evict_compact_ragged(void* k_cache, void* v_cache, float* score, int32_t* pos, const int64_t* seq_base,
+                                const int32_t* cap, const int32_t* len, const int32_t* budget,
+                                const int32_t* next_pos, int64_t total, int32_t n_seqs, int32_t n_sink,
+                                int32_t n_recent, int32_t* kept_pos_out, int32_t* new_len_out, int32_t* status,
+                                int32_t n_layers, int32_t kv_heads, int32_t d, int32_t dtype, void* workspace,
+                                size_t ws_bytes, void* stream) {
+    static const char* fn = "voxzip_evict_compact_ragged";
+    if (!k_cache || !v_cache || !score || !pos || !seq_base || !cap || !len || !budget || !next_pos)
+        return fail(VZ_ERR_INVALID, fn, "null pointer");
+    int rc = check_ragged(fn, n_layers, kv_heads, d, dtype, total, n_seqs);
+    if (rc) return rc;
+    if (n_sink < 0) return fail(VZ_ERR_INVALID, fn, "n_sink must be >= 0");
+    if (new_len_out && overlaps(new_len_out, 4 * static_cast<size_t>(n_seqs), len, 4 * static_cast<size_t>(n_seqs)))
+        return fail(VZ_ERR_INVALID, fn, "new_len_out must not overlap len");
+    const size_t need = vz_evict_ws_bytes(n_layers, total, n_seqs);
+    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    VzRagged rg{seq_base, cap, len, next_pos, budget, status, n_seqs, total};
+    VzEvictArgs a{k_cache, v_cache, score, pos, 0, 0, n_sink, n_recent, 0, kept_pos_out,
+                  n_layers, kv_heads, d, 0, dtype, workspace, ws_bytes, rg, new_len_out};
     hipError_t e = vz_launch_evict(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
 }
 
 }  // extern "C"
 
-size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap) {
+size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int64_t plane, int32_t n_seqs) {
     (void)Hkv;
     (void)d;
-    const size_t gen = vz_decode_generic_ws_bytes(L, Hq, cap);
-    const size_t fused = vz_decode_fused_ws_bytes(L, Hq, cap);
+    const size_t gen = vz_decode_generic_ws_bytes(L, Hq, plane, n_seqs);
+    const size_t fused = vz_decode_fused_ws_bytes(L, Hq, plane, n_seqs);
     return gen > fused ? gen : fused;
 }
 
 hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream) {
-    if (vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.cap, a.L)) return vz_launch_decode_fused(a, stream);
+    const int64_t plane = a.rag.n > 0 ? a.rag.total : a.cap;
+    if (vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.L, plane, a.rag.n)) return vz_launch_decode_fused(a, stream);
+    if (!vz_decode_generic_ok(plane, a.rag.n)) return hipErrorInvalidValue;
     return vz_launch_decode_generic(a, stream);
 }

@@ -51,7 +51,6 @@ constexpr int CHUNK = 16 * TILES;      // keys per chunk (at most)
 constexpr int VT = 32;                 // keys per staged tile
 constexpr int KSTEPS = D / 32;         // MFMA k-steps over the channels
 constexpr int DTILES = D / 16;         // output column tiles
-constexpr int MAX_CHUNKS = 512;        // chunks per layer served here
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kRor8 = 0x128;           // DPP row_ror:8 (swap the halves of each 16-lane row)
 constexpr int kBufferDword3 = 0x00020000;  // raw buffer descriptor word 3 (32-bit data format)
@@ -71,7 +70,8 @@ constexpr size_t kHeaderBytes = 256;  // decode workspace header (unused by this
 //   ml [L][nc_max][Hq]        float2     chunk max m_c and sum l_c of exp2, per head
 //   o  [L][nc_max][Hq][D]     bfloat16   O_c relative to m_c
 //   p  [L][nc_max][Hq][CHUNK] half       p~ = exp2(s - m_c) per key of the chunk
-//   layer [L][Hq]             float2     the layer's max M and 1 / sum S, per head
+//   layer [S][L][Hq]          float2     the layer's max M and 1 / sum S, per head
+//                                        (S = sequences of the call)
 template <typename B>
 struct PartialsT {
     using F2 = typename std::conditional<std::is_const<B>::value, const float2, float2>::type;
@@ -91,15 +91,9 @@ struct PartialsT {
 using Partials = PartialsT<uint8_t>;
 using ConstPartials = PartialsT<const uint8_t>;
 
-size_t partials_bytes(int32_t L, int32_t nc_max, int32_t Hq) {
-    return static_cast<size_t>(L) * nc_max * Hq * (sizeof(float2) + sizeof(uint16_t) * (D + CHUNK)) +
-           static_cast<size_t>(L) * Hq * sizeof(float2);
-}
-
-// First key of chunk c of T keys split into n near-equal chunks (c <= 512 and
-// T < 2^22, checked on the host, so the product fits in 32 bits).
+// First key of chunk c of T keys split into n near-equal chunks.
 __host__ __device__ __forceinline__ int chunk_begin(int c, int T, int n) {
-    return static_cast<int>(static_cast<uint32_t>(c) * static_cast<uint32_t>(T) / static_cast<uint32_t>(n));
+    return static_cast<int>(static_cast<uint64_t>(c) * static_cast<uint64_t>(T) / static_cast<uint64_t>(n));
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
@@ -130,14 +124,73 @@ __device__ __forceinline__ float f16_to_f32(uint16_t x) {
     return static_cast<float>(h);
 }
 
-template <int NW>
-__global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
-    uint16_t* __restrict__ k_cache, uint16_t* __restrict__ v_cache, int32_t* __restrict__ pos, int32_t len,
-    int32_t next_pos, float scale_log2, int32_t Hq, int32_t cap, int32_t n_chunks, int32_t nc_max, int32_t L,
-    uint8_t* __restrict__ ws, int32_t hdr_bytes) {
-    __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][TILE_BYTES];
+// Kernel arguments shared by the three launches.  A single-sequence call
+// has rag.n == 0 and takes len, next_pos and n_chunks from here; a ragged
+// call reads them per sequence.
+struct FusedArgs {
+    const uint16_t* q;
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    uint16_t* k_cache;
+    uint16_t* v_cache;
+    int32_t* pos;
+    float* score;
+    uint16_t* out;
+    uint8_t* ws;
+    int32_t len, next_pos;  // single sequence
+    int32_t n_chunks;       // single sequence
+    int32_t nc_max;         // chunk rows of the partials per layer (grid bound for a ragged call)
+    int32_t Hq, L, hdr_bytes;
+    int64_t plane;          // slots per (layer, KV head) plane
+    float scale_log2, gamma;
+    VzRagged rag;
+};
 
+// Chunks of sequence s in a ragged call (0 when it cannot be served).
+__device__ __forceinline__ int ragged_chunks(const VzRagged& r, int s) {
+    return vz::ragged_decode_status(r, s) == VZ_OK ? (r.len[s] + CHUNK) / CHUNK : 0;
+}
+
+// The sequence a work item belongs to, resolved at the top of every kernel.
+struct SeqItem {
+    int s;           // sequence (0 for a single-sequence call)
+    int len, next_pos;
+    int n_chunks;    // chunks of the sequence
+    int first;       // its first chunk row in the partials
+    int64_t base;    // its first slot in the planes
+};
+
+// Flat chunk f of a call: false when it holds no work.
+template <bool RAG>
+__device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem& it, int& c) {
+    if constexpr (RAG) {
+        int first = 0, nc = 0;
+        const int s = vz::ragged_locate(f, a.rag.n, a.nc_max, [&](int t) { return ragged_chunks(a.rag, t); },
+                                        first, nc);
+        if (s < 0 || first + nc > a.nc_max) return false;
+        it.s = s;
+        it.len = __builtin_amdgcn_readfirstlane(a.rag.len[s]);
+        it.next_pos = __builtin_amdgcn_readfirstlane(a.rag.next_pos[s]);
+        it.n_chunks = nc;
+        it.first = first;
+        it.base = a.rag.base[s];
+        c = f - first;
+    } else {
+        if (f >= a.n_chunks) return false;
+        it.s = 0;
+        it.len = a.len;
+        it.next_pos = a.next_pos;
+        it.n_chunks = a.n_chunks;
+        it.first = 0;
+        it.base = 0;
+        c = f;
+    }
+    return true;
+}
+
+template <int NW, bool RAG>
+__global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(const FusedArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][TILE_BYTES];
     const int tid = threadIdx.x;
     // wave-uniform values go through readfirstlane so that addresses built
     // from them stay scalar (buffer descriptors in SGPRs)
@@ -145,31 +198,39 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
     const int q4 = lane >> 4, r16 = lane & 15;
     const int hi = r16 >> 3;          // 0: even tile of a pair, 1: odd tile (packed lanes)
     const int hh = r16 & 7;           // query head of the group this lane's logits belong to
+    const int Hq = a.Hq, nc_max = a.nc_max;
     const int G = Hq / NW;
     const int g = w;                  // KV head of this wave
 
-    Partials part(ws, hdr_bytes, L, nc_max, Hq);
+    Partials part(a.ws, a.hdr_bytes, a.L, nc_max, Hq);
     const int item = blockIdx.x;
-    const int l = item / n_chunks, c = item - (item / n_chunks) * n_chunks;
+    const int per_layer = RAG ? nc_max : a.n_chunks;
+    const int l = item / per_layer;
+    SeqItem it;
+    int c;
+    if (!resolve_chunk<RAG>(a, item - l * per_layer, it, c)) return;
+    const int len = it.len;
     const int T = len + 1;
+    const int n_chunks = it.n_chunks;
     const int k_begin = chunk_begin(c, T, n_chunks);
     const int nk = chunk_begin(c + 1, T, n_chunks) - k_begin;
-    const size_t head_base = (static_cast<size_t>(l) * NW + g) * static_cast<size_t>(cap) * D;
-    uint16_t* Kh = k_cache + head_base;
-    uint16_t* Vh = v_cache + head_base;
+    const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base) * D;
+    uint16_t* Kh = a.k_cache + head_base;
+    uint16_t* Vh = a.v_cache + head_base;
+    const size_t row_sl = static_cast<size_t>(it.s) * a.L + l;  // (sequence, layer) row of q, out, k_new, v_new
 
     // Eq. (1) first: the chunk holding slot len writes the new row into the
     // cache (the wave of each KV head its own row, complete before its loads),
     // so every key is read from the cache the same way.
     if (len >= k_begin && len < k_begin + nk) {
-        const uint16_t* kn = k_new + (l * NW + g) * D;
-        const uint16_t* vn = v_new + (l * NW + g) * D;
+        const uint16_t* kn = a.k_new + (row_sl * NW + g) * D;
+        const uint16_t* vn = a.v_new + (row_sl * NW + g) * D;
         if (lane < 16)
             *reinterpret_cast<uint4*>(Kh + len * D + 8 * lane) = *reinterpret_cast<const uint4*>(kn + 8 * lane);
         else if (lane < 32)
             *reinterpret_cast<uint4*>(Vh + len * D + 8 * (lane - 16)) =
                 *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
-        if (tid == 0) pos[l * cap + len] = next_pos;
+        if (tid == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
         __threadfence_block();
     }
 
@@ -212,7 +273,7 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
     uint4 qv[KSTEPS];  // B operand: Q^T, column r16 = query head (zero past G)
     {
         const int hq = r16 < G ? r16 : 0;
-        const uint16_t* qrow = q + (l * Hq + g * G + hq) * D + 8 * q4;
+        const uint16_t* qrow = a.q + (row_sl * Hq + g * G + hq) * D + 8 * q4;
 #pragma unroll
         for (int s = 0; s < KSTEPS; ++s) {
             const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * s);
@@ -244,7 +305,7 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
             const float odd = ror8(acc[1][i]);  // lane hi=1 receives the odd tile of head hh
             const float v = hi ? odd : acc[0][i];
             const int key = VT * u + 16 * hi + 4 * q4 + i;
-            sp[u][i] = (key < nk) ? v * scale_log2 : -INFINITY;
+            sp[u][i] = (key < nk) ? v * a.scale_log2 : -INFINITY;
         }
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
@@ -270,7 +331,7 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
     l_c += __shfl_xor(l_c, 16, 64);
     l_c += __shfl_xor(l_c, 32, 64);
     l_c += ror8(l_c);
-    const int pbase = (l * nc_max + c) * Hq + g * G;  // < 2^31 (checked on the host)
+    const int pbase = (l * nc_max + it.first + c) * Hq + g * G;  // < 2^31 (checked on the host)
     if (q4 == 0 && r16 < G) part.ml[pbase + r16] = make_float2(m_c, l_c);
 
     // ---------------- pass 2: O^T = V^T P^T on the matrix cores ----------------
@@ -348,28 +409,39 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(
     }
 }
 
-// Output kernel, one workgroup of 256 threads per (head h, layer l).  Thread
-// t owns channels 8 (t % 16) .. +7 of the rows of chunks t / 16, t / 16 + 16,
-// ...: it merges them with a running max, o = sum_c O_c exp2(m_c - M) /
-// sum_c l_c exp2(m_c - M), and the 16 row groups then merge in LDS.  All
-// loads of a round (16-byte row pieces and the chunk pairs) are issued before
-// any use: indexes past the end are clamped and the values masked afterwards,
-// so no load sits behind a branch.  Also stores the layer's (max, 1 / sum) of
-// head h for the fold kernel.
+// Output kernel, one workgroup of 256 threads per (head h, layer l,
+// sequence).  Thread t owns channels 8 (t % 16) .. +7 of the rows of chunks
+// t / 16, t / 16 + 16, ...: it merges them with a running max,
+// o = sum_c O_c exp2(m_c - M) / sum_c l_c exp2(m_c - M), and the 16 row groups
+// then merge in LDS.  All loads of a round (16-byte row pieces and the chunk
+// pairs) are issued before any use: indexes past the end are clamped and the
+// values masked afterwards, so no load sits behind a branch.  Also stores the
+// layer's (max, 1 / sum) of head h for the fold kernel and, in a ragged call,
+// the sequence's status.
 constexpr int OUT_THREADS = 256;
 constexpr int OUT_ROWS = OUT_THREADS / 16;  // row groups
 constexpr int OUT_BATCH = 8;                // chunks per row group and round
-__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(uint8_t* __restrict__ ws,
-                                                                   uint16_t* __restrict__ out, int32_t Hq,
-                                                                   int32_t n_chunks, int32_t nc_max, int32_t L,
-                                                                   int32_t hdr_bytes) {
+template <bool RAG>
+__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedArgs a) {
     __shared__ float s_acc[OUT_ROWS][D + 4];
     __shared__ float s_m[OUT_ROWS], s_l[OUT_ROWS];
     const int h = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    const int Hq = a.Hq;
     const int rg = t / 16, c8 = 8 * (t % 16);
-    Partials part(ws, hdr_bytes, L, nc_max, Hq);
-    const float2* ml = part.ml + static_cast<size_t>(l) * nc_max * Hq + h;
-    const uint16_t* po = part.o + (static_cast<size_t>(l) * nc_max * Hq + h) * D + c8;
+    int s = 0, first = 0, n_chunks = a.n_chunks;
+    if constexpr (RAG) {
+        s = blockIdx.z;
+        const int st = vz::ragged_decode_status(a.rag, s);
+        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
+        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
+        const bool ok = st == VZ_OK && first >= 0 && first + n_chunks <= a.nc_max;
+        if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[s] = ok ? VZ_OK : (st != VZ_OK ? st : VZ_ERR_CAPACITY);
+        if (!ok) return;
+    }
+    Partials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
+    const size_t row0 = static_cast<size_t>(l) * a.nc_max + first;  // first chunk row of (layer, sequence)
+    const float2* ml = part.ml + row0 * Hq + h;
+    const uint16_t* po = part.o + (row0 * Hq + h) * D + c8;
     float M = -INFINITY, S = 0.f, acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.f;
@@ -411,41 +483,45 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(uint8_t* __r
         float Mg = s_m[0];
 #pragma unroll
         for (int r = 1; r < OUT_ROWS; ++r) Mg = fmaxf(Mg, s_m[r]);
-        float a = 0.f, sum = 0.f;
+        float o = 0.f, sum = 0.f;
 #pragma unroll
         for (int r = 0; r < OUT_ROWS; ++r) {
             const float f = s_m[r] == -INFINITY ? 0.f : exp2f(s_m[r] - Mg);
-            a += s_acc[r][t] * f;
+            o += s_acc[r][t] * f;
             sum += s_l[r] * f;
         }
         const float il = 1.0f / sum;
-        out[(static_cast<size_t>(l) * Hq + h) * D + t] = vz::f32_to_bf16(a * il);
-        if (t == 0) part.layer[static_cast<size_t>(l) * Hq + h] = make_float2(Mg, il);
+        const size_t row_sl = static_cast<size_t>(s) * a.L + l;
+        a.out[(row_sl * Hq + h) * D + t] = vz::f32_to_bf16(o * il);
+        if (t == 0) part.layer[row_sl * Hq + h] = make_float2(Mg, il);
     }
 }
 
-// Fold kernel, one workgroup of CHUNK threads per (chunk c, layer l), thread
-// = key: Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h with
+// Fold kernel, one workgroup of CHUNK threads per (chunk, layer), thread =
+// key: Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h with
 // f_h = exp2(m_c,h - M_h) / S_h (the new slot starts from 0).  Heads go in
 // rounds of 32: the round's p~ loads and factor loads are issued together
 // (p~ rows are complete, CHUNK entries each, so every load is in bounds;
 // heads past Hq are clamped and masked, so no load sits behind a branch).
 constexpr int FOLD_HEADS = 32;
-__global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const uint8_t* __restrict__ ws, float* __restrict__ score,
-                                                            int32_t len, float gamma, int32_t Hq, int32_t cap,
-                                                            int32_t n_chunks, int32_t nc_max, int32_t L,
-                                                            int32_t hdr_bytes) {
+template <bool RAG>
+__global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
     __shared__ float s_f[FOLD_HEADS];
-    const int c = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
-    const ConstPartials part(ws, hdr_bytes, L, nc_max, Hq);
-    const int T = len + 1;
-    const int k_begin = chunk_begin(c, T, n_chunks);
-    const int nk = chunk_begin(c + 1, T, n_chunks) - k_begin;
+    const int l = blockIdx.y, t = threadIdx.x;
+    const int Hq = a.Hq;
+    SeqItem it;
+    int c;
+    if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) return;
+    const ConstPartials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
+    const int len = it.len, T = len + 1;
+    const int k_begin = chunk_begin(c, T, it.n_chunks);
+    const int nk = chunk_begin(c + 1, T, it.n_chunks) - k_begin;
     const int j = k_begin + (t < nk ? t : 0);
-    float* a = score + static_cast<size_t>(l) * cap + j;
-    const float a_ld = *a;
+    float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
+    const float a_ld = *sc;
     const float a_old = (t < nk && j < len) ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
-    const size_t cbase = (static_cast<size_t>(l) * nc_max + c) * Hq;
+    const size_t cbase = (static_cast<size_t>(l) * a.nc_max + it.first + c) * Hq;
+    const float2* layer = part.layer + (static_cast<size_t>(it.s) * a.L + l) * Hq;
     const uint16_t* pp = part.p + cbase * CHUNK + t;
     float acc = 0.f;
     for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
@@ -453,7 +529,7 @@ __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const uint8_t* __res
 #pragma unroll
         for (int k = 0; k < FOLD_HEADS; ++k) pr[k] = pp[min(hb + k, Hq - 1) * CHUNK];
         if (t < FOLD_HEADS && hb + t < Hq) {
-            const float2 gl = part.layer[static_cast<size_t>(l) * Hq + hb + t];
+            const float2 gl = layer[hb + t];
             s_f[t] = exp2f(part.ml[cbase + hb + t].x - gl.x) * gl.y;
         }
         __syncthreads();
@@ -462,33 +538,60 @@ __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const uint8_t* __res
             if (hb + k < Hq) acc += f16_to_f32(pr[k]) * s_f[k];
         __syncthreads();
     }
-    if (t < nk) *a = gamma * a_old + acc;
+    if (t < nk) *sc = a.gamma * a_old + acc;
 }
 
-int32_t fused_chunks(int32_t T) { return (T + CHUNK - 1) / CHUNK; }
+int32_t fused_chunks(int64_t T) { return static_cast<int32_t>((T + CHUNK - 1) / CHUNK); }
 
-template <int NW>
-hipError_t launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
-    const int T = a.len + 1;
-    const int n_chunks = fused_chunks(T);
-    const int nc_max = fused_chunks(a.cap);
-    const float scale = (a.sm_scale > 0.f ? a.sm_scale : 1.0f / sqrtf(static_cast<float>(D))) * kLog2e;
-    const int hdr = static_cast<int>(vz_decode_hdr_bytes(a.L));
-    auto* ws = static_cast<uint8_t*>(a.ws);
-    hipLaunchKernelGGL((decode_attend_kernel<NW>), dim3(a.L * n_chunks), dim3(64 * NW), 0, stream,
-                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k_new),
-                       static_cast<const uint16_t*>(a.v_new), static_cast<uint16_t*>(a.k_cache),
-                       static_cast<uint16_t*>(a.v_cache), a.pos, a.len, a.next_pos, scale, a.Hq, a.cap, n_chunks,
-                       nc_max, a.L, ws, hdr);
+// Chunk rows of the partials per layer of a ragged call: a bound on the sum of
+// ceil((len[s] + 1) / CHUNK) over sequences that lie inside the planes
+// without overlapping (each holds at most cap[s] <= its share of `total` slots).
+int32_t ragged_chunk_rows(int64_t total, int32_t n_seqs) { return fused_chunks(total) + n_seqs; }
+
+template <int NW, bool RAG>
+hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
+    FusedArgs a{};
+    a.q = static_cast<const uint16_t*>(v.q);
+    a.k_new = static_cast<const uint16_t*>(v.k_new);
+    a.v_new = static_cast<const uint16_t*>(v.v_new);
+    a.k_cache = static_cast<uint16_t*>(v.k_cache);
+    a.v_cache = static_cast<uint16_t*>(v.v_cache);
+    a.pos = v.pos;
+    a.score = v.score;
+    a.out = static_cast<uint16_t*>(v.out);
+    a.ws = static_cast<uint8_t*>(v.ws);
+    a.Hq = v.Hq;
+    a.L = v.L;
+    a.hdr_bytes = static_cast<int32_t>(vz_decode_hdr_bytes(v.L));
+    a.scale_log2 = (v.sm_scale > 0.f ? v.sm_scale : 1.0f / sqrtf(static_cast<float>(D))) * kLog2e;
+    a.gamma = v.gamma;
+    a.rag = v.rag;
+    int seqs = 1;
+    if (RAG) {
+        a.plane = v.rag.total;
+        a.nc_max = ragged_chunk_rows(v.rag.total, v.rag.n);
+        a.n_chunks = a.nc_max;  // grid extent per layer
+        seqs = v.rag.n;
+    } else {
+        a.plane = v.cap;
+        a.len = v.len;
+        a.next_pos = v.next_pos;
+        a.n_chunks = fused_chunks(static_cast<int64_t>(v.len) + 1);
+        a.nc_max = fused_chunks(v.cap);
+    }
+    hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_output_kernel, dim3(a.Hq, a.L), dim3(OUT_THREADS), 0, stream, ws,
-                       static_cast<uint16_t*>(a.out), a.Hq, n_chunks, nc_max, a.L, hdr);
+    hipLaunchKernelGGL((decode_output_kernel<RAG>), dim3(a.Hq, a.L, seqs), dim3(OUT_THREADS), 0, stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_fold_kernel, dim3(n_chunks, a.L), dim3(CHUNK), 0, stream, ws, a.score, a.len, a.gamma,
-                       a.Hq, a.cap, n_chunks, nc_max, a.L, hdr);
+    hipLaunchKernelGGL((decode_fold_kernel<RAG>), dim3(a.n_chunks, a.L), dim3(CHUNK), 0, stream, a);
     return hipGetLastError();
+}
+
+template <int NW>
+hipError_t launch_decode_fused_any(const VzDecodeArgs& v, hipStream_t stream) {
+    return v.rag.n > 0 ? launch_decode_fused<NW, true>(v, stream) : launch_decode_fused<NW, false>(v, stream);
 }
 
 }  // namespace
@@ -499,31 +602,33 @@ size_t vz_decode_hdr_bytes(int32_t L) {
     return kHeaderBytes;
 }
 
-bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap, int32_t L) {
+namespace {
+int64_t chunk_rows(int64_t plane, int32_t n_seqs) {
+    return n_seqs > 0 ? ragged_chunk_rows(plane, n_seqs) : fused_chunks(plane);
+}
+}  // namespace
+
+bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t L, int64_t plane, int32_t n_seqs) {
     if (dtype != VZ_BF16 || d != D) return false;
     if (!(Hkv == 1 || Hkv == 2 || Hkv == 4 || Hkv == 8)) return false;
     if (Hq % Hkv != 0 || Hq / Hkv > GMAX) return false;
-    const int64_t ncm = fused_chunks(cap);
-    if (ncm > MAX_CHUNKS) return false;
-    // 32-bit offsets inside the kernels: partials, scores, positions, outputs,
-    // one head's rows, chunk bounds
-    if (static_cast<int64_t>(L) * ncm * Hq * CHUNK >= (int64_t(1) << 31)) return false;
-    if (static_cast<int64_t>(L) * cap >= (int64_t(1) << 31)) return false;
-    if (static_cast<int64_t>(cap) * D * 2 >= (int64_t(1) << 31)) return false;
-    if (static_cast<int64_t>(L) * Hq * D >= (int64_t(1) << 31)) return false;
-    return static_cast<int64_t>(cap) < (int64_t(1) << 22);
+    // 32-bit chunk-row indexes of the partials (the attend grid is smaller)
+    return static_cast<int64_t>(L) * chunk_rows(plane, n_seqs) * Hq < (int64_t(1) << 31);
 }
 
-size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int32_t cap) {
-    return vz_decode_hdr_bytes(L) + partials_bytes(L, fused_chunks(cap), Hq);
+size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs) {
+    const int64_t rows = chunk_rows(plane, n_seqs);
+    const int32_t seqs = n_seqs > 0 ? n_seqs : 1;
+    return vz_decode_hdr_bytes(L) + static_cast<size_t>(L) * rows * Hq * (sizeof(float2) + sizeof(uint16_t) * (D + CHUNK)) +
+           static_cast<size_t>(seqs) * L * Hq * sizeof(float2);
 }
 
 hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
     switch (a.Hkv) {
-        case 1: return launch_decode_fused<1>(a, stream);
-        case 2: return launch_decode_fused<2>(a, stream);
-        case 4: return launch_decode_fused<4>(a, stream);
-        case 8: return launch_decode_fused<8>(a, stream);
+        case 1: return launch_decode_fused_any<1>(a, stream);
+        case 2: return launch_decode_fused_any<2>(a, stream);
+        case 4: return launch_decode_fused_any<4>(a, stream);
+        case 8: return launch_decode_fused_any<8>(a, stream);
         default: return hipErrorInvalidValue;
     }
 }

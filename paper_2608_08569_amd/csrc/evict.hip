@@ -35,9 +35,11 @@ constexpr int kBitmapWords = 8192;  // kept-position bitmap: 2^18 positions
 constexpr int kLdsSlots = 16384;    // slots whose keys fit in LDS
 constexpr uint64_t kNoKey = ~0ull;  // LDS key of a slot that does not compete
 
-// Block-shared state; the kept-position bitmap is its own array unless the
-// LDS key array (free by then) holds it.
-template <bool OWN_BITMAP>
+// Block-shared state of the select kernels.  KEYS: the rank keys of the
+// layer's slots fit in LDS (kNoKey for sinks and recent slots); the
+// kept-position bitmap then aliases the key array (free by the time the bitmap
+// is built), otherwise it is an array of its own.
+template <bool KEYS>
 struct SelShared {
     uint64_t red64[kSelWaves];
     int red_a[kSelWaves];
@@ -46,8 +48,14 @@ struct SelShared {
     uint64_t prefix;
     int krem;
     int cnt;
-    uint32_t bitmap[OWN_BITMAP ? kBitmapWords : 1];
+    int32_t ev[kSmallE];  // slots of the evicted keys found by the rounds (keys in LDS only)
+    int nm;
+    int32_t src[kInlineRows], dst[kInlineRows];  // move lists (keys in LDS only)
+    uint64_t keys[KEYS ? kLdsSlots : 1];
+    uint32_t own_bitmap[KEYS ? 1 : kBitmapWords];
+    __device__ uint32_t* bitmap() { return KEYS ? reinterpret_cast<uint32_t*>(keys) : own_bitmap; }
 };
+static_assert(kLdsSlots * 2 >= kBitmapWords, "the key array holds the bitmap");
 
 template <class SH>
 __device__ uint64_t block_min_u64(uint64_t v, SH& sh) {
@@ -98,27 +106,44 @@ __device__ void block_scan2(int a, int b, int& ax, int& bx, int& at, int& bt, SH
     bt = tb;
 }
 
-template <int DT, int D, bool LK>
-__global__ __launch_bounds__(kSel) void select_kernel(
-    typename vz::Elem<DT>::T* __restrict__ k_cache, typename vz::Elem<DT>::T* __restrict__ v_cache,
-    float* __restrict__ score, int32_t* __restrict__ pos, int32_t len, int32_t budget, int32_t n_sink,
-    int32_t M, int32_t next_pos, int32_t* __restrict__ kept_pos_out, int32_t Hkv, int32_t cap,
-    int32_t* __restrict__ ws_n, int32_t* __restrict__ ws_src, int32_t* __restrict__ ws_dst, int inline_kv) {
+// One layer of one sequence: the slots of its planes start at A, P (score,
+// position) and k0, v0 (row 0 of KV head 0; head h is head_stride elements
+// further).  src_g / dst_g: global move lists (used when LK is false);
+// n_out: receives the number of moves left for the copy kernel; kept: NULL or
+// the layer's kept-position output.
+template <class T>
+struct SelJob {
+    float* A;
+    int32_t* P;
+    T* k0;
+    T* v0;
+    size_t head_stride;
+    int32_t* src_g;
+    int32_t* dst_g;
+    int32_t* n_out;
+    int32_t* kept;
+    int32_t len, budget, n_sink, M, next_pos, Hkv;
+    int inline_kv;
+};
+
+// LK: this layer's keys are kept in LDS (needs sh.keys and len <= kLdsSlots
+// and inline_kv).
+template <int DT, int D, bool LK, class SH>
+__device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh) {
     using T = typename vz::Elem<DT>::T;
     constexpr int PER = vz::Elem<DT>::kPer16B;
     constexpr int CH = D / PER;
-    __shared__ SelShared<!LK> sh;
-    // LK: the rank keys of the layer's slots (kNoKey for sinks and recent
-    // slots) and the move lists live in LDS
-    __shared__ uint64_t s_keys[LK ? kLdsSlots : 1];
-    static_assert(!LK || kLdsSlots * 2 >= kBitmapWords, "the key array holds the bitmap");
-    uint32_t* const bitmap = LK ? reinterpret_cast<uint32_t*>(s_keys) : sh.bitmap;
-    __shared__ int32_t s_src[LK ? kInlineRows : 1], s_dst[LK ? kInlineRows : 1];
+    uint64_t* const s_keys = sh.keys;
+    uint32_t* const bitmap = sh.bitmap();
+    int32_t* const s_src = sh.src;
+    int32_t* const s_dst = sh.dst;
+    int32_t* const s_ev = sh.ev;
 
-    const int l = blockIdx.x;
     const int tid = threadIdx.x;
-    float* A = score + static_cast<size_t>(l) * cap;
-    int32_t* P = pos + static_cast<size_t>(l) * cap;
+    float* A = job.A;
+    int32_t* P = job.P;
+    const int len = job.len, budget = job.budget, n_sink = job.n_sink, M = job.M, next_pos = job.next_pos;
+    const int Hkv = job.Hkv;
     const int E = len > budget ? len - budget : 0;
     const int32_t recent_from = next_pos - M;
     auto is_mid = [&](int32_t p) { return p >= n_sink && p < recent_from; };
@@ -158,9 +183,6 @@ __global__ __launch_bounds__(kSel) void select_kernel(
     // ---- threshold: evict middle slots whose key >> shift <= thr >> shift ----
     uint64_t thr = 0;
     int shift = 0;
-    // slots of the evicted keys, found by the rounds below (LK only)
-    __shared__ int32_t s_ev[LK ? kSmallE : 1];
-    __shared__ int s_nm;
     if (E > 0 && E <= kSmallE) {
         uint64_t tau = 0;
         int found = 0;
@@ -208,7 +230,7 @@ __global__ __launch_bounds__(kSel) void select_kernel(
                         ++nm;
                     }
                 }
-                s_nm = nm;
+                sh.nm = nm;
             }
             __syncthreads();
         }
@@ -269,11 +291,11 @@ __global__ __launch_bounds__(kSel) void select_kernel(
     }
 
     // ---- holes (evicted, slot < budget) and movers (kept, slot >= budget) ----
-    int32_t* src = LK ? s_src : ws_src + static_cast<size_t>(l) * cap;
-    int32_t* dst = LK ? s_dst : ws_dst + static_cast<size_t>(l) * cap;
+    int32_t* src = LK ? s_src : job.src_g;
+    int32_t* dst = LK ? s_dst : job.dst_g;
     int n_moves = 0;
     if (LK && E > 0 && E <= kSmallE) {
-        n_moves = s_nm;  // paired above
+        n_moves = sh.nm;  // paired above
     } else {
         const int per = (len + kSel - 1) / kSel;
         const int j0 = min(tid * per, len), j1 = min(j0 + per, len);
@@ -300,7 +322,6 @@ __global__ __launch_bounds__(kSel) void select_kernel(
             }
         }
         n_moves = min(ht, mt);
-        if (!LK && tid == 0) ws_n[l] = n_moves;
         __syncthreads();
     }
 
@@ -309,7 +330,8 @@ __global__ __launch_bounds__(kSel) void select_kernel(
         A[d] = A[s];
         P[d] = P[s];
     }
-    if (LK || inline_kv) {
+    if (tid == 0) *job.n_out = (LK || job.inline_kv) ? 0 : n_moves;
+    if (LK || job.inline_kv) {
         const int total = n_moves * Hkv * 2 * CH;
         for (int i = tid; i < total; i += kSel) {
             const int c = i % CH;
@@ -317,13 +339,13 @@ __global__ __launch_bounds__(kSel) void select_kernel(
             const int which = t & 1;
             t >>= 1;
             const int h = t % Hkv, r = t / Hkv;
-            T* base = (which ? v_cache : k_cache) + (static_cast<size_t>(l) * Hkv + h) * cap * D + c * PER;
+            T* base = (which ? job.v0 : job.k0) + h * job.head_stride + c * PER;
             *reinterpret_cast<uint4*>(base + static_cast<size_t>(dst[r]) * D) =
                 *reinterpret_cast<const uint4*>(base + static_cast<size_t>(src[r]) * D);
         }
     }
 
-    if (kept_pos_out) {
+    if (job.kept) {
         __syncthreads();
         const int new_len = E > 0 ? budget : len;
         const int words = (next_pos + 31) / 32;
@@ -340,7 +362,7 @@ __global__ __launch_bounds__(kSel) void select_kernel(
         for (int w = w0; w < w1; ++w) c += __popc(bitmap[w]);
         int cx, dummy, ct, dt;
         block_scan2(c, 0, cx, dummy, ct, dt, sh);
-        int32_t* outp = kept_pos_out + static_cast<size_t>(l) * budget;
+        int32_t* outp = job.kept;
         for (int w = w0; w < w1; ++w) {
             uint32_t bits = bitmap[w];
             while (bits) {
@@ -353,66 +375,189 @@ __global__ __launch_bounds__(kSel) void select_kernel(
     }
 }
 
+// Single sequence: one block per layer.
+template <int DT, int D, bool LK>
+__global__ __launch_bounds__(kSel) void select_kernel(const VzEvictArgs a, int32_t M, int32_t* __restrict__ ws_n,
+                                                      int32_t* __restrict__ ws_src, int32_t* __restrict__ ws_dst,
+                                                      int inline_kv) {
+    using T = typename vz::Elem<DT>::T;
+    __shared__ SelShared<LK> sh;
+    const int l = blockIdx.x;
+    const size_t row = static_cast<size_t>(l) * a.cap;
+    SelJob<T> job;
+    job.A = a.score + row;
+    job.P = a.pos + row;
+    job.k0 = static_cast<T*>(a.k_cache) + row * a.Hkv * D;
+    job.v0 = static_cast<T*>(a.v_cache) + row * a.Hkv * D;
+    job.head_stride = static_cast<size_t>(a.cap) * D;
+    job.src_g = ws_src + row;
+    job.dst_g = ws_dst + row;
+    job.n_out = ws_n + l;
+    job.kept = a.kept_pos_out ? a.kept_pos_out + static_cast<size_t>(l) * a.budget : nullptr;
+    job.len = a.len;
+    job.budget = a.budget;
+    job.n_sink = a.n_sink;
+    job.M = M;
+    job.next_pos = a.next_pos;
+    job.Hkv = a.Hkv;
+    job.inline_kv = inline_kv;
+    select_body<DT, D, LK>(job, sh);
+}
+
+// Status of sequence s for an eviction (VZ_OK when it can be served).
+__device__ int ragged_evict_status(const VzRagged& r, int s, int n_sink, int n_recent, bool kept) {
+    const int64_t b = r.base[s];
+    const int c = r.cap[s], n = r.len[s], B = r.budget[s], p = r.next_pos[s];
+    if (n < 0 || c < 1 || b < 0 || b > r.total - c) return VZ_ERR_INVALID;
+    if (n > c) return VZ_ERR_CAPACITY;
+    const int M = n_recent < 0 ? B / 5 : n_recent;
+    if (B < 1 || static_cast<int64_t>(n_sink) + M > B || p < n) return VZ_ERR_INVALID;
+    if (kept && p > (1 << 18)) return VZ_ERR_UNSUPPORTED;
+    return VZ_OK;
+}
+
+// Ragged batch: one block per (layer, sequence).  The keys go to LDS when the
+// sequence's slots fit and few rows move, as in the single-sequence launch;
+// every block leaves its copy-kernel count in ws_n (0 when nothing is left).
 template <int DT, int D>
-__global__ __launch_bounds__(256) void compact_kernel(typename vz::Elem<DT>::T* __restrict__ k_cache,
-                                                      typename vz::Elem<DT>::T* __restrict__ v_cache,
-                                                      const int32_t* __restrict__ ws_n,
+__global__ __launch_bounds__(kSel) void select_ragged_kernel(const VzEvictArgs a, int32_t* __restrict__ ws_n,
+                                                             int32_t* __restrict__ ws_src,
+                                                             int32_t* __restrict__ ws_dst) {
+    using T = typename vz::Elem<DT>::T;
+    __shared__ SelShared<true> sh;
+    const int l = blockIdx.x, s = blockIdx.y;
+    const VzRagged& r = a.rag;
+    int32_t* const n_out = ws_n + static_cast<size_t>(s) * a.L + l;
+    const int st = ragged_evict_status(r, s, a.n_sink, a.n_recent, a.kept_pos_out != nullptr);
+    if (l == 0 && threadIdx.x == 0) {
+        if (r.status) r.status[s] = st;
+        if (a.new_len_out) {
+            const int n = r.len[s], B = r.budget[s];
+            a.new_len_out[s] = st == VZ_OK && n > B ? B : n;
+        }
+    }
+    if (st != VZ_OK) {
+        if (threadIdx.x == 0) *n_out = 0;
+        return;
+    }
+    const int len = r.len[s], budget = r.budget[s];
+    const int E = len > budget ? len - budget : 0;
+    if (E == 0 && a.kept_pos_out == nullptr) {
+        if (threadIdx.x == 0) *n_out = 0;
+        return;
+    }
+    const size_t row = static_cast<size_t>(l) * r.total + r.base[s];
+    SelJob<T> job;
+    job.A = a.score + row;
+    job.P = a.pos + row;
+    job.k0 = static_cast<T*>(a.k_cache) + (static_cast<size_t>(l) * a.Hkv * r.total + r.base[s]) * D;
+    job.v0 = static_cast<T*>(a.v_cache) + (static_cast<size_t>(l) * a.Hkv * r.total + r.base[s]) * D;
+    job.head_stride = static_cast<size_t>(r.total) * D;
+    job.src_g = ws_src + row;
+    job.dst_g = ws_dst + row;
+    job.n_out = n_out;
+    job.kept = a.kept_pos_out ? a.kept_pos_out + row : nullptr;
+    job.len = len;
+    job.budget = budget;
+    job.n_sink = a.n_sink;
+    job.M = a.n_recent < 0 ? budget / 5 : a.n_recent;
+    job.next_pos = r.next_pos[s];
+    job.Hkv = a.Hkv;
+    job.inline_kv = E <= kInlineRows ? 1 : 0;
+    if (job.inline_kv && len <= kLdsSlots)
+        select_body<DT, D, true>(job, sh);
+    else
+        select_body<DT, D, false>(job, sh);
+}
+
+// Copy kernel for layers with many moved rows: grid (jobs, y); job x =
+// (sequence, layer) (the layer alone for a single sequence), whose gridDim.y
+// blocks split its moves.
+template <int DT, int D, bool RAG>
+__global__ __launch_bounds__(256) void compact_kernel(const VzEvictArgs a, const int32_t* __restrict__ ws_n,
                                                       const int32_t* __restrict__ ws_src,
-                                                      const int32_t* __restrict__ ws_dst, int32_t Hkv, int32_t cap) {
+                                                      const int32_t* __restrict__ ws_dst) {
     using T = typename vz::Elem<DT>::T;
     constexpr int PER = vz::Elem<DT>::kPer16B;
     constexpr int CH = D / PER;
-    const int l = blockIdx.y;
-    const int n = ws_n[l];
-    const int32_t* src = ws_src + static_cast<size_t>(l) * cap;
-    const int32_t* dst = ws_dst + static_cast<size_t>(l) * cap;
-    const int64_t total = static_cast<int64_t>(n) * Hkv * 2 * CH;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < total;
-         i += static_cast<int64_t>(gridDim.x) * 256) {
+    const int job = blockIdx.x;
+    const int n = ws_n[job];
+    if (n == 0) return;
+    const int l = RAG ? job % a.L : job;
+    const int64_t plane = RAG ? a.rag.total : a.cap;
+    const int64_t base = RAG ? a.rag.base[job / a.L] : 0;
+    const size_t row = static_cast<size_t>(l) * plane + base;
+    const int32_t* src = ws_src + row;
+    const int32_t* dst = ws_dst + row;
+    const int64_t total = static_cast<int64_t>(n) * a.Hkv * 2 * CH;
+    for (int64_t i = static_cast<int64_t>(blockIdx.y) * 256 + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.y) * 256) {
         const int c = static_cast<int>(i % CH);
         int64_t t = i / CH;
         const int which = static_cast<int>(t & 1);
         t >>= 1;
-        const int h = static_cast<int>(t % Hkv);
-        const int r = static_cast<int>(t / Hkv);
-        T* base = (which ? v_cache : k_cache) + (static_cast<size_t>(l) * Hkv + h) * cap * D + c * PER;
-        *reinterpret_cast<uint4*>(base + static_cast<size_t>(dst[r]) * D) =
-            *reinterpret_cast<const uint4*>(base + static_cast<size_t>(src[r]) * D);
+        const int h = static_cast<int>(t % a.Hkv);
+        const int r = static_cast<int>(t / a.Hkv);
+        T* hb = static_cast<T*>(which ? a.v_cache : a.k_cache) +
+                ((static_cast<size_t>(l) * a.Hkv + h) * plane + base) * D + c * PER;
+        *reinterpret_cast<uint4*>(hb + static_cast<size_t>(dst[r]) * D) =
+            *reinterpret_cast<const uint4*>(hb + static_cast<size_t>(src[r]) * D);
     }
 }
 
+// Workspace: move counts [jobs rounded up to 64], then source and destination
+// lists [L][plane] each.
+struct EvictWs {
+    int32_t* n;
+    int32_t* src;
+    int32_t* dst;
+    EvictWs(void* ws, int64_t jobs, int32_t L, int64_t plane) {
+        n = static_cast<int32_t*>(ws);
+        src = n + 64 * ((jobs + 63) / 64);
+        dst = src + static_cast<size_t>(L) * plane;
+    }
+};
+
 template <int DT, int D>
 hipError_t launch(const VzEvictArgs& a, hipStream_t stream) {
-    using T = typename vz::Elem<DT>::T;
     constexpr int CH = D / vz::Elem<DT>::kPer16B;
+    if (a.rag.n > 0) {
+        const int64_t jobs = static_cast<int64_t>(a.rag.n) * a.L;
+        EvictWs w(a.ws, jobs, a.L, a.rag.total);
+        hipLaunchKernelGGL((select_ragged_kernel<DT, D>), dim3(a.L, a.rag.n), dim3(kSel), 0, stream, a, w.n, w.src,
+                           w.dst);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        // most jobs move their rows in the select block and leave 0 here
+        const int gy = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(64, 4096 / jobs)));
+        hipLaunchKernelGGL((compact_kernel<DT, D, true>), dim3(static_cast<unsigned>(jobs), gy), dim3(256), 0,
+                           stream, a, w.n, w.src, w.dst);
+        return hipGetLastError();
+    }
     const int E = a.len > a.budget ? a.len - a.budget : 0;
     if (E == 0 && a.kept_pos_out == nullptr) return hipSuccess;
-    int32_t* ws_n = static_cast<int32_t*>(a.ws);
-    int32_t* ws_src = ws_n + 64 * ((a.L + 63) / 64);
-    int32_t* ws_dst = ws_src + static_cast<size_t>(a.L) * a.cap;
+    EvictWs w(a.ws, a.L, a.L, a.cap);
     const int M = a.n_recent < 0 ? a.budget / 5 : a.n_recent;
     const int inline_kv = E <= kInlineRows ? 1 : 0;
     if (inline_kv && a.len <= kLdsSlots)
-        hipLaunchKernelGGL((select_kernel<DT, D, true>), dim3(a.L), dim3(kSel), 0, stream, static_cast<T*>(a.k_cache),
-                           static_cast<T*>(a.v_cache), a.score, a.pos, a.len, a.budget, a.n_sink, M, a.next_pos,
-                           a.kept_pos_out, a.Hkv, a.cap, ws_n, ws_src, ws_dst, inline_kv);
+        hipLaunchKernelGGL((select_kernel<DT, D, true>), dim3(a.L), dim3(kSel), 0, stream, a, M, w.n, w.src, w.dst,
+                           inline_kv);
     else
-        hipLaunchKernelGGL((select_kernel<DT, D, false>), dim3(a.L), dim3(kSel), 0, stream,
-                           static_cast<T*>(a.k_cache), static_cast<T*>(a.v_cache), a.score, a.pos, a.len, a.budget,
-                           a.n_sink, M, a.next_pos, a.kept_pos_out, a.Hkv, a.cap, ws_n, ws_src, ws_dst, inline_kv);
+        hipLaunchKernelGGL((select_kernel<DT, D, false>), dim3(a.L), dim3(kSel), 0, stream, a, M, w.n, w.src, w.dst,
+                           inline_kv);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || inline_kv) return e;
     const int64_t chunks = static_cast<int64_t>(E) * a.Hkv * 2 * CH;
-    const int gx = static_cast<int>(std::min<int64_t>((chunks + 255) / 256, 2048));
-    hipLaunchKernelGGL((compact_kernel<DT, D>), dim3(gx, a.L), dim3(256), 0, stream, static_cast<T*>(a.k_cache),
-                       static_cast<T*>(a.v_cache), ws_n, ws_src, ws_dst, a.Hkv, a.cap);
+    const int gy = static_cast<int>(std::min<int64_t>((chunks + 255) / 256, 2048));
+    hipLaunchKernelGGL((compact_kernel<DT, D, false>), dim3(a.L, gy), dim3(256), 0, stream, a, w.n, w.src, w.dst);
     return hipGetLastError();
 }
 
 }  // namespace
 
-size_t vz_evict_ws_bytes(int32_t L, int32_t /*Hkv*/, int32_t /*d*/, int32_t cap) {
-    return (static_cast<size_t>(64) * ((L + 63) / 64) + 2 * static_cast<size_t>(L) * cap) * sizeof(int32_t);
+size_t vz_evict_ws_bytes(int32_t L, int64_t plane, int32_t n_seqs) {
+    const int64_t jobs = static_cast<int64_t>(n_seqs > 0 ? n_seqs : 1) * L;
+    return (static_cast<size_t>(64) * ((jobs + 63) / 64) + 2 * static_cast<size_t>(L) * plane) * sizeof(int32_t);
 }
 
 hipError_t vz_launch_evict(const VzEvictArgs& a, hipStream_t stream) {

@@ -119,6 +119,87 @@ __device__ __forceinline__ int wave_sum_i(int v) {
 
 }  // namespace vz
 
+// ---- ragged batches ---------------------------------------------------------
+// Sequence s of a ragged batch owns slots base[s] .. base[s] + cap[s] - 1 of
+// every (layer, head) plane, and a plane holds `total` slots.  The
+// per-sequence values are device arrays read by the kernels; a sequence whose
+// values are out of range is skipped (nothing of it is read or written) and
+// its status entry says why.
+struct VzRagged {
+    const int64_t* base;
+    const int32_t* cap;
+    const int32_t* len;
+    const int32_t* next_pos;
+    const int32_t* budget;  // eviction only
+    int32_t* status;        // [n], may be null
+    int32_t n;
+    int64_t total;
+};
+
+// Largest plane (slots) and batch a ragged call serves: every flat chunk index
+// and running count below stays far from 2^31.
+constexpr int64_t kRaggedMaxTotal = int64_t(1) << 26;
+constexpr int32_t kRaggedMaxSeqs = 1 << 15;  // also a grid dimension
+
+namespace vz {
+
+// Status of sequence s for a decode step: VZ_OK when slot len[s] exists and
+// the sequence lies inside the planes.
+__device__ __forceinline__ int ragged_decode_status(const VzRagged& r, int s) {
+    const int64_t b = r.base[s];
+    const int c = r.cap[s], n = r.len[s], p = r.next_pos[s];
+    if (n < 0 || p < 0 || c < 1 || b < 0 || b > r.total - c) return VZ_ERR_INVALID;
+    if (n >= c) return VZ_ERR_CAPACITY;  // no free slot (len + 1 > cap, without overflow)
+    return VZ_OK;
+}
+
+// Flat work items of a ragged batch: sequence s contributes count(s) >= 0
+// consecutive items, in sequence order.  Called by a whole wave (every lane
+// gets the same result, wave-uniform).  Returns the sequence holding flat item
+// f, with its first flat item and its item count, or -1 when f lies past
+// `limit` items or past the last one.  count() must return at most 2^24.
+template <class Count>
+__device__ int ragged_locate(int f, int n_seqs, int limit, Count count, int& first, int& nc) {
+    const int lane = threadIdx.x % kWave;
+    int run = 0;
+    for (int s0 = 0; s0 < n_seqs && run <= limit; s0 += kWave) {
+        const int s = s0 + lane;
+        const int n0 = count(s < n_seqs ? s : n_seqs - 1);  // load for every lane, mask after
+        const int n = s < n_seqs ? n0 : 0;
+        int incl = n;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int t = __shfl_up(incl, o, kWave);
+            if (lane >= o) incl += t;
+        }
+        const unsigned long long hit = __ballot(run + incl > f);
+        if (hit) {
+            const int src = __builtin_ctzll(hit);
+            nc = __builtin_amdgcn_readfirstlane(__shfl(n, src, kWave));
+            first = __builtin_amdgcn_readfirstlane(run + __shfl(incl, src, kWave) - nc);
+            return __builtin_amdgcn_readfirstlane(s0 + src);
+        }
+        run += __shfl(incl, kWave - 1, kWave);
+    }
+    return -1;
+}
+
+// First flat item of sequence t (items as in ragged_locate), or -1 when it
+// lies past `limit`.  Called by a whole wave.
+template <class Count>
+__device__ int ragged_first(int t, int limit, Count count) {
+    const int lane = threadIdx.x % kWave;
+    int run = 0;
+    for (int s0 = 0; s0 < t && run <= limit; s0 += kWave) {
+        const int s = s0 + lane;
+        const int n0 = count(s < t ? s : t - 1);
+        run += wave_sum_i(s < t ? n0 : 0);
+    }
+    return run <= limit ? __builtin_amdgcn_readfirstlane(run) : -1;
+}
+
+}  // namespace vz
+
 // ---- launchers (one per kernel family), called by the host API -------------
 struct VzDecodeArgs {
     const void* q; const void* k_new; const void* v_new;
@@ -126,6 +207,9 @@ struct VzDecodeArgs {
     int32_t len, next_pos; float gamma, sm_scale;
     int32_t L, Hq, Hkv, d, cap, dtype;
     void* ws; size_t ws_bytes;
+    // ragged batch (rag.n > 0): len, next_pos and cap above are unused; q, out
+    // are [n][L][Hq][d], k_new, v_new [n][L][Hkv][d], planes hold rag.total slots
+    VzRagged rag;
 };
 
 struct VzEvictArgs {
@@ -134,6 +218,11 @@ struct VzEvictArgs {
     int32_t* kept_pos_out;
     int32_t L, Hkv, d, cap, dtype;
     void* ws; size_t ws_bytes;
+    // ragged batch (rag.n > 0): len, budget, next_pos and cap above are unused;
+    // kept_pos_out is [L][rag.total] (sequence s from slot base[s]); new_len_out
+    // receives min(len, budget) per sequence
+    VzRagged rag;
+    int32_t* new_len_out;
 };
 
 // Stage-1 span offsets (host); arguments checked by the caller; returns the
@@ -145,15 +234,29 @@ hipError_t vz_launch_fuse(const void* k_in, const void* v_in, int32_t T_in, cons
                           int32_t n_spans, const void* ak, const void* av, void* k_out, void* v_out,
                           float* score_out, int32_t* pos_out, int32_t L, int32_t H, int32_t d,
                           int32_t cap_out, int32_t dtype, hipStream_t stream);
-size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap);
-// decode workspace: a header (ticket, error flag) of vz_decode_hdr_bytes(L)
-// bytes, then path-specific scratch
+struct VzFuseRaggedArgs {
+    const void* k_in; const void* v_in;
+    const int64_t* in_base; const int32_t* T_in;
+    const int32_t* span_off; const int64_t* off_base; const int32_t* n_spans;
+    const void* anchor_k; const void* anchor_v;
+    void* k_out; void* v_out; float* score_out; int32_t* pos_out;
+    const int64_t* seq_base; const int32_t* cap; int32_t* status;
+    int32_t n_seqs; int64_t total_in, total_off, total; int32_t max_spans;
+    int32_t L, Hkv, d, dtype;
+};
+hipError_t vz_launch_fuse_ragged(const VzFuseRaggedArgs& a, hipStream_t stream);
+// Decode sizing: plane = slots per (layer, KV head) plane (cap, or the total
+// of a ragged batch); n_seqs = 0 for a single sequence.
+size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int64_t plane, int32_t n_seqs);
+// decode workspace: a header of vz_decode_hdr_bytes(L) bytes, then
+// path-specific scratch
 size_t vz_decode_hdr_bytes(int32_t L);
-bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t cap, int32_t L);
-size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
+bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t L, int64_t plane, int32_t n_seqs);
+size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream);
-size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int32_t cap);
+bool vz_decode_generic_ok(int64_t plane, int32_t n_seqs);
+size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_decode_generic(const VzDecodeArgs& a, hipStream_t stream);
 hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream);
-size_t vz_evict_ws_bytes(int32_t L, int32_t Hkv, int32_t d, int32_t cap);
+size_t vz_evict_ws_bytes(int32_t L, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_evict(const VzEvictArgs& a, hipStream_t stream);

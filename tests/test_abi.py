@@ -141,3 +141,94 @@ def test_binding_has_no_cpu_path():
     with pytest.raises(ValueError):
         vz.voxzip_fuse_spans(x, x, torch.zeros(2, dtype=torch.int32), x, x, torch.zeros(1, 4),
                              torch.zeros(1, 4, dtype=torch.int32))
+
+
+# ---- ragged twins: host-side rejections (no HIP call on these paths) ----
+
+def _decode_ragged(**kw):
+    a = dict(q=FAKE, kn=FAKE, vn=FAKE, kc=FAKE, vc=FAKE, s=FAKE, p=FAKE, o=FAKE, base=FAKE, cap=FAKE, len=FAKE,
+             nxt=FAKE, total=4096, n=4, gamma=0.95, scale=0.0, L=2, Hq=32, Hkv=4, d=128, dtype=vz.VZ_BF16,
+             status=None, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return vz.lib().voxzip_decode_attend_score_ragged(
+        a["q"], a["kn"], a["vn"], a["kc"], a["vc"], a["s"], a["p"], a["o"], a["base"], a["cap"], a["len"],
+        a["nxt"], a["total"], a["n"], a["gamma"], a["scale"], a["L"], a["Hq"], a["Hkv"], a["d"], a["dtype"],
+        a["status"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(len=None), vz.VZ_ERR_INVALID),
+    (dict(base=None), vz.VZ_ERR_INVALID),
+    (dict(gamma=2.0), vz.VZ_ERR_INVALID),
+    (dict(n=0), vz.VZ_ERR_SHAPE),
+    (dict(n=40000), vz.VZ_ERR_SHAPE),
+    (dict(total=0), vz.VZ_ERR_SHAPE),
+    (dict(total=(1 << 26) + 1), vz.VZ_ERR_SHAPE),
+    (dict(Hq=30), vz.VZ_ERR_SHAPE),
+    (dict(d=96), vz.VZ_ERR_UNSUPPORTED),
+    (dict(L=70000), vz.VZ_ERR_UNSUPPORTED),
+    (dict(ws_bytes=64), vz.VZ_ERR_WORKSPACE),
+])
+def test_decode_ragged_rejects(kw, code):
+    assert _decode_ragged(**kw) == code
+    assert vz.lib().voxzip_last_error().decode().startswith("voxzip_decode_attend_score_ragged")
+
+
+def _evict_ragged(**kw):
+    a = dict(kc=FAKE, vc=FAKE, s=FAKE, p=FAKE, base=FAKE, cap=FAKE, len=ctypes.c_void_p(0x20000), budget=FAKE,
+             nxt=FAKE, total=4096, n=4, n_sink=4, n_recent=-1, kept=None, new_len=None, status=None, L=2, Hkv=4,
+             d=128, dtype=vz.VZ_BF16, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return vz.lib().voxzip_evict_compact_ragged(
+        a["kc"], a["vc"], a["s"], a["p"], a["base"], a["cap"], a["len"], a["budget"], a["nxt"], a["total"], a["n"],
+        a["n_sink"], a["n_recent"], a["kept"], a["new_len"], a["status"], a["L"], a["Hkv"], a["d"], a["dtype"],
+        a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(budget=None), vz.VZ_ERR_INVALID),
+    (dict(n_sink=-1), vz.VZ_ERR_INVALID),
+    (dict(new_len=ctypes.c_void_p(0x20000 + 8)), vz.VZ_ERR_INVALID),   # overlaps len
+    (dict(n=0), vz.VZ_ERR_SHAPE),
+    (dict(dtype=5), vz.VZ_ERR_UNSUPPORTED),
+    (dict(ws=None), vz.VZ_ERR_WORKSPACE),
+])
+def test_evict_ragged_rejects(kw, code):
+    assert _evict_ragged(**kw) == code
+
+
+def _fuse_ragged(**kw):
+    a = dict(ki=ctypes.c_void_p(0x100000), vi=ctypes.c_void_p(0x200000), ib=FAKE, T=FAKE, total_in=100, off=FAKE,
+             ob=FAKE, ns=FAKE, total_off=50, max_spans=30, ak=None, av=None, ko=ctypes.c_void_p(0x400000),
+             vo=ctypes.c_void_p(0x800000), so=FAKE, po=FAKE, base=FAKE, cap=FAKE, total=64, n=2, status=None,
+             L=1, H=1, d=64, dtype=vz.VZ_F32)
+    a.update(kw)
+    return vz.lib().voxzip_fuse_spans_ragged(
+        a["ki"], a["vi"], a["ib"], a["T"], a["total_in"], a["off"], a["ob"], a["ns"], a["total_off"],
+        a["max_spans"], a["ak"], a["av"], a["ko"], a["vo"], a["so"], a["po"], a["base"], a["cap"], a["total"],
+        a["n"], a["status"], a["L"], a["H"], a["d"], a["dtype"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(ob=None), vz.VZ_ERR_INVALID),
+    (dict(ak=FAKE), vz.VZ_ERR_INVALID),
+    (dict(ko=ctypes.c_void_p(0x100000 + 64)), vz.VZ_ERR_INVALID),   # k_out inside k_in
+    (dict(max_spans=-1), vz.VZ_ERR_SHAPE),
+    (dict(max_spans=65), vz.VZ_ERR_SHAPE),                          # more spans than output slots
+    (dict(total_off=0), vz.VZ_ERR_SHAPE),
+    (dict(n=0), vz.VZ_ERR_SHAPE),
+    (dict(d=100), vz.VZ_ERR_UNSUPPORTED),
+])
+def test_fuse_ragged_rejects(kw, code):
+    assert _fuse_ragged(**kw) == code
+
+
+def test_ragged_workspace_sizes():
+    L = vz.lib()
+    one = L.voxzip_workspace_bytes(vz.VZ_OP_DECODE, 48, 32, 4, 128, 8210)
+    rag = L.voxzip_workspace_bytes_ragged(vz.VZ_OP_DECODE, 48, 32, 4, 128, 8210, 1)
+    assert rag >= one > 0
+    assert L.voxzip_workspace_bytes_ragged(vz.VZ_OP_EVICT, 48, 32, 4, 128, 80000, 16) > 0
+    assert L.voxzip_workspace_bytes_ragged(vz.VZ_OP_DECODE, 48, 32, 4, 128, 80000, 0) == 0
+    assert L.voxzip_workspace_bytes_ragged(vz.VZ_OP_DECODE, 48, 32, 4, 128, 1 << 27, 4) == 0
+    assert L.voxzip_workspace_bytes_ragged(7, 48, 32, 4, 128, 80000, 16) == 0
