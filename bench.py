@@ -168,30 +168,127 @@ class Sequence:
         return b
 
 
+class RaggedBatch:
+    """All sequences of the batched workload in one packed cache, driven
+    through the ragged entry points: one fusion call per request, one decode
+    call per step for every sequence, one eviction call every `interval`
+    steps.  Inputs are drawn exactly as for Sequence (same seeds), then packed;
+    lengths live on the device (the host mirrors them only to count bytes)."""
+
+    def __init__(self, torch, vz, ws_, steps):
+        self.torch, self.vz, self.ws_ = torch, vz, ws_
+        w = ws_[0]
+        L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+        bf = torch.bfloat16
+        n = len(ws_)
+        offs = [synth.offsets_from_lengths(synth.span_lengths(x, seq=i)) for i, x in enumerate(ws_)]
+        self.n_spans = np.array([len(o) - 1 for o in offs], dtype=np.int64)
+        self.budget = np.array([x.budget for x in ws_], dtype=np.int64)
+        T_in = np.array([x.n_audio + x.n_text for x in ws_], dtype=np.int64)
+        caps = np.maximum(self.n_spans, self.budget) + w.interval + 1
+        in_base = np.concatenate([[0], np.cumsum(T_in)[:-1]]).astype(np.int64)
+        base = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+        off_base = np.concatenate([[0], np.cumsum(self.n_spans + 1)[:-1]]).astype(np.int64)
+        self.total = int(caps.sum())
+        self.k_in = torch.empty(L, Hkv, int(T_in.sum()), d, dtype=bf, device="cuda")
+        self.v_in = torch.empty_like(self.k_in)
+        self.q = [torch.empty(n, L, Hq, d, dtype=bf, device="cuda") for _ in range(steps)]
+        self.kn = [torch.empty(n, L, Hkv, d, dtype=bf, device="cuda") for _ in range(steps)]
+        self.vn = [torch.empty(n, L, Hkv, d, dtype=bf, device="cuda") for _ in range(steps)]
+        for i, x in enumerate(ws_):
+            gen = torch.Generator(device="cuda")
+            gen.manual_seed(synth.stream_key(x.seed, x.name, "bench", i) & 0x7FFFFFFFFFFFFFFF)
+            rn = lambda *shape: torch.randn(*shape, generator=gen, device="cuda", dtype=torch.float32).to(bf)
+            sl = slice(int(in_base[i]), int(in_base[i] + T_in[i]))
+            self.k_in[:, :, sl] = rn(L, Hkv, int(T_in[i]), d)
+            self.v_in[:, :, sl] = rn(L, Hkv, int(T_in[i]), d)
+            for t in range(steps):
+                self.q[t][i] = torch.randn(L, Hq, d, generator=gen, device="cuda").to(bf)
+                self.kn[t][i] = rn(L, Hkv, d)
+                self.vn[t][i] = rn(L, Hkv, d)
+        dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a).astype(dt)).cuda()
+        self.off = dev(np.concatenate(offs), np.int32)
+        self.in_base, self.T_in, self.off_base = dev(in_base, np.int64), dev(T_in, np.int32), dev(off_base, np.int64)
+        self.n_spans_d, self.base, self.cap = dev(self.n_spans, np.int32), dev(base, np.int64), dev(caps, np.int32)
+        self.budget_d = dev(self.budget, np.int32)
+        self.K = torch.zeros(L, Hkv, self.total, d, dtype=bf, device="cuda")
+        self.V = torch.zeros_like(self.K)
+        self.S = torch.zeros(L, self.total, dtype=torch.float32, device="cuda")
+        self.P = torch.zeros(L, self.total, dtype=torch.int32, device="cuda")
+        self.out = torch.zeros(n, L, Hq, d, dtype=bf, device="cuda")
+        self.len_d = torch.zeros(n, dtype=torch.int32, device="cuda")
+        self.nxt_d = torch.zeros_like(self.len_d)
+        self.new_len = torch.zeros_like(self.len_d)
+        self.ws_d = vz.workspace_ragged(vz.VZ_OP_DECODE, L, Hq, Hkv, d, self.total, n)
+        self.ws_e = vz.workspace_ragged(vz.VZ_OP_EVICT, L, Hq, Hkv, d, self.total, n)
+
+    def start(self):
+        vz = self.vz
+        vz.voxzip_fuse_spans_ragged(self.k_in, self.v_in, self.in_base, self.T_in, self.off, self.off_base,
+                                    self.n_spans_d, int(self.n_spans.max()), self.K, self.V, self.S, self.P,
+                                    self.base, self.cap)
+        self.len_d.copy_(self.n_spans_d)
+        self.nxt_d.copy_(self.n_spans_d)
+        self.len = self.n_spans.copy()
+
+    def step(self, t):
+        """Decode step t of every sequence (and the eviction when it is due);
+        returns the algorithmic bytes."""
+        w, vz = self.ws_[0], self.vz
+        L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+        vz.voxzip_decode_attend_score_ragged(self.q[t], self.kn[t], self.vn[t], self.K, self.V, self.S, self.P,
+                                             self.out, self.base, self.cap, self.len_d, self.nxt_d, w.gamma,
+                                             workspace=self.ws_d)
+        T = self.len + 1
+        b = sum(L * decode_bytes_per_layer(int(x), Hq, Hkv, d, 2) for x in T)
+        self.len = T
+        self.len_d += 1
+        self.nxt_d += 1
+        if (t + 1) % w.interval == 0:
+            vz.voxzip_evict_compact_ragged(self.K, self.V, self.S, self.P, self.base, self.cap, self.len_d,
+                                           self.budget_d, self.nxt_d, new_len_out=self.new_len,
+                                           workspace=self.ws_e)
+            self.len_d.copy_(self.new_len)
+            E = np.maximum(self.len - self.budget, 0)
+            b += sum(L * evict_bytes_per_layer(int(x), int(e), Hkv, d, 2) for x, e in zip(T, E) if e > 0)
+            self.len = np.minimum(self.len, self.budget)
+        return b
+
+
 def other_workload(args, torch, vz):
     """aggr64k (one sequence, 512 steps) or batch16 (16 sequences of 2k-32k
-    tokens on 16 streams, 128 steps each, eviction every 16 steps): whole
-    requests (fusion + all steps), tokens/s over the wall clock and the
-    algorithmic bytes of the path per second."""
+    tokens, 128 steps each, eviction every 16 steps; through the ragged entry
+    points, or with --batch-streams one call sequence per sequence on 16
+    streams): whole requests (fusion + all steps), tokens/s over the wall
+    clock and the algorithmic bytes of the path per second."""
     if args.workload == "aggr64k":
         ws_ = [synth.workload("aggr64k")]
     else:
         ws_ = synth.batch_workloads()
     steps = ws_[0].steps
     t0 = time.time()
-    seqs = [Sequence(torch, vz, w, i, steps, torch.cuda.Stream()) for i, w in enumerate(ws_)]
+    ragged = args.workload == "batch16" and not args.batch_streams
+    if ragged:
+        batch = RaggedBatch(torch, vz, ws_, steps)
+        n_seqs, n_spans = len(ws_), int(batch.n_spans.sum())
+    else:
+        seqs = [Sequence(torch, vz, w, i, steps, torch.cuda.Stream()) for i, w in enumerate(ws_)]
+        n_seqs, n_spans = len(seqs), sum(s.n for s in seqs)
     torch.cuda.synchronize()
-    log(f"[gpu] {args.workload}: {len(seqs)} sequence(s), {sum(s.n for s in seqs)} spans, "
-        f"inputs ready in {time.time() - t0:.1f}s")
+    log(f"[gpu] {args.workload}: {n_seqs} sequence(s), {n_spans} spans, inputs ready in {time.time() - t0:.1f}s")
 
     def request():
+        if ragged:
+            batch.start()
+            b = sum(batch.step(t) for t in range(steps))
+            return n_seqs * steps, b
         b = 0
         for s in seqs:
             s.start()
         for t in range(steps):
             for s in seqs:
                 b += s.step(t)
-        return len(seqs) * steps, b
+        return n_seqs * steps, b
 
     for _ in range(args.warmup):
         request()
@@ -210,16 +307,18 @@ def other_workload(args, torch, vz):
                 f"length 1) fused to {seqs[0].n} spans, B=3277, queries biased to about 5 percent of the keys, "
                 f"512 decode steps with eviction")
     else:
-        lens = "/".join(str(s.w.n_audio) for s in seqs)
+        lens = "/".join(str(x.n_audio) for x in ws_)
+        how = ("one packed cache, one ragged decode call per step for all sequences" if ragged
+               else "one HIP stream and one call sequence per sequence")
         desc = (f"16 sequences of {lens} audio tokens (spans of mean length 4), budget len/4 each, eviction "
-                f"every 16 steps, 128 decode steps each; one HIP stream per sequence")
+                f"every 16 steps, 128 decode steps each; {how}")
     print(json.dumps({
         "metric": "decode attend+score+evict tokens/s and HBM GB/s (% of peak)",
         "value": tokens / elapsed, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": elapsed * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "description": desc, "layers": w.n_layers,
-                   "sequences": len(seqs), "decode_steps_per_request": steps},
+                   "sequences": n_seqs, "decode_steps_per_request": steps},
         "path_gbps": path_bytes / elapsed / 1e9,
         "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
     }), flush=True)
@@ -238,6 +337,8 @@ def main():
                     help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--workload", default="long32k", choices=["long32k", "aggr64k", "batch16"],
                     help="long32k is the headline; the others are reported beside it")
+    ap.add_argument("--batch-streams", action="store_true",
+                    help="batch16 with one stream and one call sequence per sequence instead of the ragged calls")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
