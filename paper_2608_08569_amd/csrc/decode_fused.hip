@@ -48,6 +48,7 @@ constexpr int GMAX = 8;                // query heads per KV head served here
 constexpr int TILES = 8;               // 16-key MFMA tiles per chunk
 constexpr int PAIRS = TILES / 2;       // packed tile pairs = 32-key tiles
 constexpr int CHUNK = 16 * TILES;      // keys per chunk (at most)
+constexpr int ATTEND_WG_PER_CU = 4;   // resident attend workgroups per CU (128 VGPRs)
 constexpr int VT = 32;                 // keys per staged tile
 constexpr int KSTEPS = D / 32;         // MFMA k-steps over the channels
 constexpr int DTILES = D / 16;         // output column tiles
@@ -189,7 +190,7 @@ __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem
 }
 
 template <int NW, bool RAG>
-__global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(const FusedArgs a) {
+__global__ __launch_bounds__(64 * NW, ATTEND_WG_PER_CU) void decode_attend_kernel(const FusedArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][TILE_BYTES];
     const int tid = threadIdx.x;
     // wave-uniform values go through readfirstlane so that addresses built
@@ -374,18 +375,20 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(const FusedAr
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
     // ---------------- partial results: whole rows through LDS ----------------
-    // p~ (half) and O (bfloat16, relative to the chunk max) of the wave's G
-    // heads are staged in its free tile buffer, 256 bytes per head at a
-    // 320-byte stride, then written as 1 KB fully coalesced stores: the
-    // workspace holds both as rows of 256 bytes, heads of the wave adjacent.
+    // p~ (half, CHUNK entries per head) and O (bfloat16 relative to the chunk
+    // max, 256 bytes per head) of the wave's G heads are staged in its free
+    // tile buffer at padded per-head strides, then written as 1 KB fully
+    // coalesced stores: the workspace holds both as rows, heads of the wave
+    // adjacent.
     {
-        constexpr int HS = 320;
+        constexpr int PR = CHUNK * 2, HSP = PR + 64, HS = 256 + 64;
+        static_assert(GMAX * (HSP + HS) <= TILE_BYTES, "the staged partials fit in the tile buffer");
         uint8_t* const lp = buf;
-        uint8_t* const lo = buf + GMAX * HS;
+        uint8_t* const lo = buf + GMAX * HSP;
         if (hh < G) {
 #pragma unroll
             for (int u = 0; u < PAIRS; ++u)
-                *reinterpret_cast<uint2*>(lp + hh * HS + 2 * (VT * u + 16 * hi + 4 * q4)) =
+                *reinterpret_cast<uint2*>(lp + hh * HSP + 2 * (VT * u + 16 * hi + 4 * q4)) =
                     make_uint2(pack_f16x2(sp[u][0], sp[u][1]), pack_f16x2(sp[u][2], sp[u][3]));
         }
         if (r16 < G) {
@@ -395,50 +398,60 @@ __global__ __launch_bounds__(64 * NW, 4) void decode_attend_kernel(const FusedAr
                     make_uint2(pack_bf16x2(oacc[n][0], oacc[n][1]), pack_bf16x2(oacc[n][2], oacc[n][3]));
         }
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): staged
-        uint8_t* const gp = reinterpret_cast<uint8_t*>(part.p) + static_cast<size_t>(pbase) * (CHUNK * 2);
+        uint8_t* const gp = reinterpret_cast<uint8_t*>(part.p) + static_cast<size_t>(pbase) * PR;
         uint8_t* const go = reinterpret_cast<uint8_t*>(part.o) + static_cast<size_t>(pbase) * (D * 2);
+#pragma unroll
+        for (int j = 0; j < GMAX * PR / 1024; ++j) {
+            const int off = 1024 * j + 16 * lane;
+            if (off < G * PR)
+                *reinterpret_cast<uint4*>(gp + off) =
+                    *reinterpret_cast<const uint4*>(lp + (off / PR) * HSP + off % PR);
+        }
 #pragma unroll
         for (int j = 0; j < GMAX * 256 / 1024; ++j) {
             const int off = 1024 * j + 16 * lane;
-            if (off < G * 256) {
-                const int src = (off >> 8) * HS + (off & 255);
-                *reinterpret_cast<uint4*>(gp + off) = *reinterpret_cast<const uint4*>(lp + src);
-                *reinterpret_cast<uint4*>(go + off) = *reinterpret_cast<const uint4*>(lo + src);
-            }
+            if (off < G * 256)
+                *reinterpret_cast<uint4*>(go + off) = *reinterpret_cast<const uint4*>(lo + (off >> 8) * HS + (off & 255));
         }
     }
 }
 
-// Output kernel, one workgroup of 256 threads per (head h, layer l,
-// sequence).  Thread t owns channels 8 (t % 16) .. +7 of the rows of chunks
-// t / 16, t / 16 + 16, ...: it merges them with a running max,
-// o = sum_c O_c exp2(m_c - M) / sum_c l_c exp2(m_c - M), and the 16 row groups
-// then merge in LDS.  All loads of a round (16-byte row pieces and the chunk
-// pairs) are issued before any use: indexes past the end are clamped and the
-// values masked afterwards, so no load sits behind a branch.  Also stores the
-// layer's (max, 1 / sum) of head h for the fold kernel and, in a ragged call,
-// the sequence's status.
+// ---- finishing: merge of the chunk partials ----
+// Sums use explicit fused multiply-adds, so the bits do not depend on how the
+// compiler contracts each kernel (the single-sequence and ragged calls give
+// the same bits).
 constexpr int OUT_THREADS = 256;
 constexpr int OUT_ROWS = OUT_THREADS / 16;  // row groups
 constexpr int OUT_BATCH = 8;                // chunks per row group and round
-template <bool RAG>
-__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedArgs a) {
+
+// Merge of the OUT_ROWS row-group statistics: (layer max M, 1 / sum S).
+__device__ __forceinline__ float2 combine_rows(const float* sm, const float* sl, int stride) {
+    float Mg = sm[0];
+#pragma unroll
+    for (int r = 1; r < OUT_ROWS; ++r) Mg = fmaxf(Mg, sm[r * stride]);
+    float sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < OUT_ROWS; ++r) {
+        const float f = sm[r * stride] == -INFINITY ? 0.f : exp2f(sm[r * stride] - Mg);
+        sum = fmaf(sl[r * stride], f, sum);
+    }
+    return make_float2(Mg, 1.0f / sum);
+}
+
+// Output row of head h of (layer l, sequence s) from the sequence's n_chunks
+// partials starting at chunk row `first`, by a whole block of OUT_THREADS
+// threads.  Thread t owns channels 8 (t % 16) .. +7 of the rows of chunks
+// t / 16, t / 16 + 16, ...: a running max, o = sum_c O_c exp2(m_c - M) /
+// sum_c l_c exp2(m_c - M); the 16 row groups then merge in LDS.  All loads of
+// a round (16-byte row pieces and the chunk pairs) are issued before any use:
+// indexes past the end are clamped and the values masked afterwards.
+// Returns the layer's (max, 1 / sum) of head h in thread 0.
+__device__ float2 merge_output_row(const FusedArgs& a, const Partials& part, int h, int l, int s, int first,
+                                   int n_chunks) {
     __shared__ float s_acc[OUT_ROWS][D + 4];
     __shared__ float s_m[OUT_ROWS], s_l[OUT_ROWS];
-    const int h = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
-    const int Hq = a.Hq;
+    const int t = threadIdx.x, Hq = a.Hq;
     const int rg = t / 16, c8 = 8 * (t % 16);
-    int s = 0, first = 0, n_chunks = a.n_chunks;
-    if constexpr (RAG) {
-        s = blockIdx.z;
-        const int st = vz::ragged_decode_status(a.rag, s);
-        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
-        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
-        const bool ok = st == VZ_OK && first >= 0 && first + n_chunks <= a.nc_max;
-        if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[s] = ok ? VZ_OK : (st != VZ_OK ? st : VZ_ERR_CAPACITY);
-        if (!ok) return;
-    }
-    Partials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
     const size_t row0 = static_cast<size_t>(l) * a.nc_max + first;  // first chunk row of (layer, sequence)
     const float2* ml = part.ml + row0 * Hq + h;
     const uint16_t* po = part.o + (row0 * Hq + h) * D + c8;
@@ -468,8 +481,8 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedA
             float x[8];
             vz::unpack16<VZ_BF16>(xr[k], x);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc[i] += wgt * x[i];
-            S += wgt * st[k].y;
+            for (int i = 0; i < 8; ++i) acc[i] = fmaf(wgt, x[i], acc[i]);
+            S = fmaf(wgt, st[k].y, S);
         }
     }
 #pragma unroll
@@ -479,66 +492,91 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedA
         s_l[rg] = S;
     }
     __syncthreads();
+    float2 stats = make_float2(0.f, 0.f);
     if (t < D) {
-        float Mg = s_m[0];
-#pragma unroll
-        for (int r = 1; r < OUT_ROWS; ++r) Mg = fmaxf(Mg, s_m[r]);
-        float o = 0.f, sum = 0.f;
+        stats = combine_rows(s_m, s_l, 1);
+        float o = 0.f;
 #pragma unroll
         for (int r = 0; r < OUT_ROWS; ++r) {
-            const float f = s_m[r] == -INFINITY ? 0.f : exp2f(s_m[r] - Mg);
-            o += s_acc[r][t] * f;
-            sum += s_l[r] * f;
+            const float f = s_m[r] == -INFINITY ? 0.f : exp2f(s_m[r] - stats.x);
+            o = fmaf(s_acc[r][t], f, o);
         }
-        const float il = 1.0f / sum;
         const size_t row_sl = static_cast<size_t>(s) * a.L + l;
-        a.out[(row_sl * Hq + h) * D + t] = vz::f32_to_bf16(o * il);
-        if (t == 0) part.layer[row_sl * Hq + h] = make_float2(Mg, il);
+        a.out[(row_sl * Hq + h) * D + t] = vz::f32_to_bf16(o * stats.y);
     }
+    return stats;
 }
 
-// Fold kernel, one workgroup of CHUNK threads per (chunk, layer), thread =
-// key: Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h with
-// f_h = exp2(m_c,h - M_h) / S_h (the new slot starts from 0).  Heads go in
-// rounds of 32: the round's p~ loads and factor loads are issued together
-// (p~ rows are complete, CHUNK entries each, so every load is in bounds;
-// heads past Hq are clamped and masked, so no load sits behind a branch).
+// Fold of chunk c, key k of the chunk per thread: Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h,
+// f_h = exp2(m_c,h - M_h) / S_h given in fac[h] (the new slot starts from 0).
+// Heads go in rounds of 32 whose p~ loads are issued together (p~ rows are
+// complete, CHUNK entries each, so every load is in bounds; heads past Hq are
+// clamped and masked, so no load sits behind a branch).
 constexpr int FOLD_HEADS = 32;
+__device__ __forceinline__ void fold_chunk(const FusedArgs& a, const ConstPartials& part, const SeqItem& it, int l,
+                                           int c, int k, const float* fac) {
+    const int Hq = a.Hq;
+    const int len = it.len, T = len + 1;
+    const int k_begin = chunk_begin(c, T, it.n_chunks);
+    const int nk = chunk_begin(c + 1, T, it.n_chunks) - k_begin;
+    const int j = k_begin + (k < nk ? k : 0);
+    float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
+    const float a_ld = *sc;
+    const float a_old = (k < nk && j < len) ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
+    const size_t cbase = (static_cast<size_t>(l) * a.nc_max + it.first + c) * Hq;
+    const uint16_t* pp = part.p + cbase * CHUNK + k;
+    float acc = 0.f;
+    for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
+        uint16_t pr[FOLD_HEADS];
+#pragma unroll
+        for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(hb + q, Hq - 1) * CHUNK];
+#pragma unroll
+        for (int q = 0; q < FOLD_HEADS; ++q)
+            if (hb + q < Hq) acc = fmaf(f16_to_f32(pr[q]), fac[hb + q], acc);
+    }
+    if (k < nk) *sc = fmaf(a.gamma, a_old, acc);
+}
+
+// Output kernel, one block per (head, layer, sequence):
+// the output row, the layer's (max, 1 / sum) of the head for the fold kernel
+// and, in a ragged call, the sequence's status.
+template <bool RAG>
+__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedArgs a) {
+    const int h = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    int s = 0, first = 0, n_chunks = a.n_chunks;
+    if constexpr (RAG) {
+        s = blockIdx.z;
+        const int st = vz::ragged_decode_status(a.rag, s);
+        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
+        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
+        const bool ok = st == VZ_OK && first >= 0 && first + n_chunks <= a.nc_max;
+        if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[s] = ok ? VZ_OK : (st != VZ_OK ? st : VZ_ERR_CAPACITY);
+        if (!ok) return;
+    }
+    Partials part(a.ws, a.hdr_bytes, a.L, a.nc_max, a.Hq);
+    const float2 stats = merge_output_row(a, part, h, l, s, first, n_chunks);
+    if (t == 0) part.layer[(static_cast<size_t>(s) * a.L + l) * a.Hq + h] = stats;
+}
+
+// Fold kernel, one block of CHUNK threads per (chunk, layer), thread = key;
+// the factors come from the layer statistics the output kernel stored.
 template <bool RAG>
 __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
-    __shared__ float s_f[FOLD_HEADS];
+    __shared__ float s_f[GMAX * 8];
     const int l = blockIdx.y, t = threadIdx.x;
     const int Hq = a.Hq;
     SeqItem it;
     int c;
     if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) return;
     const ConstPartials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
-    const int len = it.len, T = len + 1;
-    const int k_begin = chunk_begin(c, T, it.n_chunks);
-    const int nk = chunk_begin(c + 1, T, it.n_chunks) - k_begin;
-    const int j = k_begin + (t < nk ? t : 0);
-    float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
-    const float a_ld = *sc;
-    const float a_old = (t < nk && j < len) ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
     const size_t cbase = (static_cast<size_t>(l) * a.nc_max + it.first + c) * Hq;
     const float2* layer = part.layer + (static_cast<size_t>(it.s) * a.L + l) * Hq;
-    const uint16_t* pp = part.p + cbase * CHUNK + t;
-    float acc = 0.f;
-    for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
-        uint16_t pr[FOLD_HEADS];
-#pragma unroll
-        for (int k = 0; k < FOLD_HEADS; ++k) pr[k] = pp[min(hb + k, Hq - 1) * CHUNK];
-        if (t < FOLD_HEADS && hb + t < Hq) {
-            const float2 gl = layer[hb + t];
-            s_f[t] = exp2f(part.ml[cbase + hb + t].x - gl.x) * gl.y;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int k = 0; k < FOLD_HEADS; ++k)
-            if (hb + k < Hq) acc += f16_to_f32(pr[k]) * s_f[k];
-        __syncthreads();
+    for (int h = t; h < Hq; h += CHUNK) {
+        const float2 gl = layer[h];
+        s_f[h] = exp2f(part.ml[cbase + h].x - gl.x) * gl.y;
     }
-    if (t < nk) *sc = a.gamma * a_old + acc;
+    __syncthreads();
+    fold_chunk(a, part, it, l, c, t, s_f);
 }
 
 int32_t fused_chunks(int64_t T) { return static_cast<int32_t>((T + CHUNK - 1) / CHUNK); }

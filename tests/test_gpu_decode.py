@@ -133,8 +133,38 @@ def test_gamma_edges_and_explicit_scale():
         assert abs(S.sum() - expect) <= 1e-4 * expect
 
 
+@pytest.mark.parametrize("length", [16383, 16384])
+def test_single_and_ragged_calls_agree_on_long_sequences(length):
+    """T = 16,384 and 16,385 keys (128 and 129 chunks): the single-sequence call
+    against the oracle and bit for bit against the ragged call on the same data."""
+    import torch
+    import paper_2608_08569_amd as vz
+    dtype, L, Hq, Hkv, d = synth.DT_BF16, 1, 32, 4, 128
+    cap = length + 2
+    k, v, s, p = synth.random_state(31, L, Hkv, d, cap, length, dtype, next_pos=length + 5)
+    w = synth.workload("layer")
+    q, kn, vn = synth.decode_inputs(w, 1)
+    g = GpuCache(L, Hq, Hkv, d, cap, dtype)
+    g.load(k, v, s, p, length, length + 5)
+    synced_step(g, q, kn, vn, 0.95)
+    K1, V1, S1, P1 = g.snapshot()
+    out1 = from_dev(g.out)
+    r = GpuCache(L, Hq, Hkv, d, cap, dtype)
+    r.load(k, v, s, p, length, length + 5)
+    dev = lambda a, dt: torch.tensor(a, dtype=dt, device="cuda")
+    ws = vz.workspace_ragged(vz.VZ_OP_DECODE, L, Hq, Hkv, d, cap, 1)
+    out = torch.zeros(1, L, Hq, d, dtype=torch.bfloat16, device="cuda")
+    vz.voxzip_decode_attend_score_ragged(to_dev(q[None]), to_dev(kn[None]), to_dev(vn[None]), r.k, r.v, r.score,
+                                         r.pos, out, dev([0], torch.int64), dev([cap], torch.int32),
+                                         dev([length], torch.int32), dev([length + 5], torch.int32), 0.95,
+                                         workspace=ws)
+    K2, V2, S2, P2 = r.snapshot()
+    assert np.array_equal(from_dev(out)[0], out1)
+    assert np.array_equal(S2, S1) and np.array_equal(P2, P1) and np.array_equal(K2, K1)
+
+
 def test_many_chunks_per_layer():
-    """65,535 resident keys: 256 chunks per layer on the fused path (its limit)."""
+    """65,535 resident keys: 512 chunks of 128 keys per layer on the fused path."""
     dtype, L, Hq, Hkv, d, length = synth.DT_BF16, 1, 32, 4, 128, 65535
     k, v, s, p = synth.random_state(12, L, Hkv, d, length + 1, length, dtype)
     g = GpuCache(L, Hq, Hkv, d, length + 1, dtype)
