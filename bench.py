@@ -324,6 +324,96 @@ def other_workload(args, torch, vz):
     }), flush=True)
 
 
+def loop_workload(args, torch, vz):
+    """long32k through the decode loop (paper_2608_08569_amd.loop): one
+    decode call per layer, layer l's query being its own input query plus
+    layer l - 1's output (the dependency of a forward pass), eviction after
+    every step; launched eagerly (long32k-layers) or replayed per token from a
+    HIP graph (long32k-graph).  Same fused cache and inputs as the headline."""
+    from paper_2608_08569_amd.loop import DecodeLoop
+    w = synth.workload("long32k")
+    L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+    t0 = time.time()
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n_spans = len(off) - 1
+    T_in = w.n_audio + w.n_text
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    k_in, v_in = bf(synth.prefill_kv(w, "k")), bf(synth.prefill_kv(w, "v"))
+    steps = args.decode_steps
+    inputs = []
+    for t in range(steps):
+        q, kn, vn = synth.decode_inputs(w, t)
+        inputs.append((bf(q).view(L, 1, 1, Hq, d), bf(kn).view(L, 1, 1, Hkv, d), bf(vn).view(L, 1, 1, Hkv, d)))
+    log(f"[gpu] {args.workload}: inputs ready in {time.time() - t0:.1f}s: {n_spans} spans")
+    cap = max(n_spans, w.budget) + 2
+    lp = DecodeLoop(L, Hq, Hkv, d, [cap], [w.budget], w.gamma, interval=1)
+    i64 = lambda v: torch.tensor(v, dtype=torch.int64, device="cuda")
+    i32 = lambda v: torch.tensor(v, dtype=torch.int32, device="cuda")
+    off_d = torch.from_numpy(off).cuda()
+    qmix = torch.zeros(L, 1, 1, Hq, d, dtype=torch.bfloat16, device="cuda")
+
+    def layer_query(l, q, outs):
+        return q[0] if l == 0 else torch.add(q[l], outs[l - 1], out=qmix[l])
+
+    graph = args.workload == "long32k-graph"
+    qb, kb, vb = (torch.zeros_like(x) for x in inputs[0])
+
+    def start():
+        lp.fuse(k_in, v_in, i64([0]), i32([T_in]), off_d, i64([0]), i32([n_spans]), n_spans)
+
+    start()
+    if graph:
+        lp.capture(qb, kb, vb, layer_query)
+
+    def request():
+        start()
+        b = 0
+        length = n_spans
+        for t in range(steps):
+            q, kn, vn = inputs[t]
+            if graph:
+                qb.copy_(q)
+                kb.copy_(kn)
+                vb.copy_(vn)
+                lp.replay()
+            else:
+                lp.step(q, kn, vn, layer_query)
+            T = length + 1
+            b += L * decode_bytes_per_layer(T, Hq, Hkv, d, 2)
+            if T > w.budget:
+                b += L * evict_bytes_per_layer(T, T - w.budget, Hkv, d, 2)
+            length = min(T, w.budget)
+        return steps, b
+
+    for _ in range(args.warmup):
+        request()
+    torch.cuda.synchronize()
+    tokens = path_bytes = 0
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        tk, b = request()
+        tokens += tk
+        path_bytes += b
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    how = "replayed per token from a HIP graph" if graph else "launched eagerly"
+    print(json.dumps({
+        "metric": "decode attend+score+evict tokens/s and HBM GB/s (% of peak)",
+        "value": tokens / elapsed, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload,
+                   "description": (f"the 32k workload ({n_spans} spans, B=8192, 48 layers, 32Q/4KV, d=128) with "
+                                   f"one decode call per layer, each layer's query depending on the previous "
+                                   f"layer's output, eviction every step, {how}; one step = fusion + "
+                                   f"{steps} decode steps"),
+                   "layers": L, "sequences": 1, "decode_steps_per_request": steps},
+        "us_per_token": elapsed * 1e6 / tokens,
+        "path_gbps": path_bytes / elapsed / 1e9,
+        "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -335,7 +425,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
-    ap.add_argument("--workload", default="long32k", choices=["long32k", "aggr64k", "batch16"],
+    ap.add_argument("--workload", default="long32k",
+                    choices=["long32k", "aggr64k", "batch16", "long32k-layers", "long32k-graph"],
                     help="long32k is the headline; the others are reported beside it")
     ap.add_argument("--batch-streams", action="store_true",
                     help="batch16 with one stream and one call sequence per sequence instead of the ragged calls")
@@ -363,6 +454,9 @@ def main():
         print(json.dumps({"copy_probe_bytes": n}))
         return
 
+    if args.workload in ("long32k-layers", "long32k-graph"):
+        loop_workload(args, torch, vz)
+        return
     if args.workload != "long32k":
         other_workload(args, torch, vz)
         return

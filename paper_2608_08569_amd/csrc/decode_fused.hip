@@ -141,6 +141,7 @@ struct FusedArgs {
     int32_t len, next_pos;  // single sequence
     int32_t n_chunks;       // single sequence
     int32_t nc_max;         // chunk rows of the partials per layer (grid bound for a ragged call)
+    int32_t chunk_keys;     // keys per chunk, at most (CHUNK, or fewer for calls with few chunks)
     int32_t Hq, L, hdr_bytes;
     int64_t plane;          // slots per (layer, KV head) plane
     float scale_log2, gamma;
@@ -148,8 +149,8 @@ struct FusedArgs {
 };
 
 // Chunks of sequence s in a ragged call (0 when it cannot be served).
-__device__ __forceinline__ int ragged_chunks(const VzRagged& r, int s) {
-    return vz::ragged_decode_status(r, s) == VZ_OK ? (r.len[s] + CHUNK) / CHUNK : 0;
+__device__ __forceinline__ int ragged_chunks(const VzRagged& r, int s, int chunk_keys) {
+    return vz::ragged_decode_status(r, s) == VZ_OK ? (r.len[s] + chunk_keys) / chunk_keys : 0;
 }
 
 // The sequence a work item belongs to, resolved at the top of every kernel.
@@ -166,7 +167,7 @@ template <bool RAG>
 __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem& it, int& c) {
     if constexpr (RAG) {
         int first = 0, nc = 0;
-        const int s = vz::ragged_locate(f, a.rag.n, a.nc_max, [&](int t) { return ragged_chunks(a.rag, t); },
+        const int s = vz::ragged_locate(f, a.rag.n, a.nc_max, [&](int t) { return ragged_chunks(a.rag, t, a.chunk_keys); },
                                         first, nc);
         if (s < 0 || first + nc > a.nc_max) return false;
         it.s = s;
@@ -507,36 +508,6 @@ __device__ float2 merge_output_row(const FusedArgs& a, const Partials& part, int
     return stats;
 }
 
-// Fold of chunk c, key k of the chunk per thread: Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h,
-// f_h = exp2(m_c,h - M_h) / S_h given in fac[h] (the new slot starts from 0).
-// Heads go in rounds of 32 whose p~ loads are issued together (p~ rows are
-// complete, CHUNK entries each, so every load is in bounds; heads past Hq are
-// clamped and masked, so no load sits behind a branch).
-constexpr int FOLD_HEADS = 32;
-__device__ __forceinline__ void fold_chunk(const FusedArgs& a, const ConstPartials& part, const SeqItem& it, int l,
-                                           int c, int k, const float* fac) {
-    const int Hq = a.Hq;
-    const int len = it.len, T = len + 1;
-    const int k_begin = chunk_begin(c, T, it.n_chunks);
-    const int nk = chunk_begin(c + 1, T, it.n_chunks) - k_begin;
-    const int j = k_begin + (k < nk ? k : 0);
-    float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
-    const float a_ld = *sc;
-    const float a_old = (k < nk && j < len) ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
-    const size_t cbase = (static_cast<size_t>(l) * a.nc_max + it.first + c) * Hq;
-    const uint16_t* pp = part.p + cbase * CHUNK + k;
-    float acc = 0.f;
-    for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
-        uint16_t pr[FOLD_HEADS];
-#pragma unroll
-        for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(hb + q, Hq - 1) * CHUNK];
-#pragma unroll
-        for (int q = 0; q < FOLD_HEADS; ++q)
-            if (hb + q < Hq) acc = fmaf(f16_to_f32(pr[q]), fac[hb + q], acc);
-    }
-    if (k < nk) *sc = fmaf(a.gamma, a_old, acc);
-}
-
 // Output kernel, one block per (head, layer, sequence):
 // the output row, the layer's (max, 1 / sum) of the head for the fold kernel
 // and, in a ragged call, the sequence's status.
@@ -547,8 +518,8 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedA
     if constexpr (RAG) {
         s = blockIdx.z;
         const int st = vz::ragged_decode_status(a.rag, s);
-        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
-        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
+        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u, a.chunk_keys); }) : -1;
+        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s, a.chunk_keys) : 0;
         const bool ok = st == VZ_OK && first >= 0 && first + n_chunks <= a.nc_max;
         if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[s] = ok ? VZ_OK : (st != VZ_OK ? st : VZ_ERR_CAPACITY);
         if (!ok) return;
@@ -558,33 +529,65 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedA
     if (t == 0) part.layer[(static_cast<size_t>(s) * a.L + l) * a.Hq + h] = stats;
 }
 
-// Fold kernel, one block of CHUNK threads per (chunk, layer), thread = key;
-// the factors come from the layer statistics the output kernel stored.
+// Fold kernel, one block of CHUNK threads per (chunk, layer), thread = key:
+// Eq. (6), A[j] = gamma A[j] + sum_h p~_hj f_h with f_h = exp2(m_c,h - M_h) / S_h
+// from the layer statistics the output kernel stored (the new slot starts
+// from 0).  Heads go in rounds of 32: the round's p~ loads are issued before
+// its factors are formed (p~ rows are complete, CHUNK entries each, so every
+// load is in bounds; heads past Hq are clamped and masked, so no load sits
+// behind a branch).
+constexpr int FOLD_HEADS = 32;
 template <bool RAG>
 __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
-    __shared__ float s_f[GMAX * 8];
+    __shared__ float s_f[FOLD_HEADS];
     const int l = blockIdx.y, t = threadIdx.x;
     const int Hq = a.Hq;
     SeqItem it;
     int c;
     if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) return;
     const ConstPartials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
+    const int len = it.len, T = len + 1;
+    const int k_begin = chunk_begin(c, T, it.n_chunks);
+    const int nk = chunk_begin(c + 1, T, it.n_chunks) - k_begin;
+    const int j = k_begin + (t < nk ? t : 0);
+    float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
+    const float a_ld = *sc;
+    const float a_old = (t < nk && j < len) ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
     const size_t cbase = (static_cast<size_t>(l) * a.nc_max + it.first + c) * Hq;
     const float2* layer = part.layer + (static_cast<size_t>(it.s) * a.L + l) * Hq;
-    for (int h = t; h < Hq; h += CHUNK) {
-        const float2 gl = layer[h];
-        s_f[h] = exp2f(part.ml[cbase + h].x - gl.x) * gl.y;
+    const uint16_t* pp = part.p + cbase * CHUNK + t;
+    float acc = 0.f;
+    for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
+        uint16_t pr[FOLD_HEADS];
+#pragma unroll
+        for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(hb + q, Hq - 1) * CHUNK];
+        if (t < FOLD_HEADS && hb + t < Hq) {
+            const float2 gl = layer[hb + t];
+            s_f[t] = exp2f(part.ml[cbase + hb + t].x - gl.x) * gl.y;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < FOLD_HEADS; ++q)
+            if (hb + q < Hq) acc = fmaf(f16_to_f32(pr[q]), s_f[q], acc);
+        __syncthreads();
     }
-    __syncthreads();
-    fold_chunk(a, part, it, l, c, t, s_f);
+    if (t < nk) *sc = fmaf(a.gamma, a_old, acc);
 }
 
-int32_t fused_chunks(int64_t T) { return static_cast<int32_t>((T + CHUNK - 1) / CHUNK); }
-
-// Chunk rows of the partials per layer of a ragged call: a bound on the sum of
-// ceil((len[s] + 1) / CHUNK) over sequences that lie inside the planes
-// without overlapping (each holds at most cap[s] <= its share of `total` slots).
-int32_t ragged_chunk_rows(int64_t total, int32_t n_seqs) { return fused_chunks(total) + n_seqs; }
+// Keys per chunk.  Smaller chunks for calls over few layers were measured and
+// do not help: a one-layer call is bound by its chain of dependent round
+// trips, not by the number of workgroups, and more chunks make the merge
+// heavier.
+int32_t chunk_keys_for(int32_t /*L*/) { return CHUNK; }
+int64_t chunk_rows_for(int64_t plane, int32_t n_seqs, int32_t ck) {
+    return (plane + ck - 1) / ck + (n_seqs > 0 ? n_seqs : 0);
+}
+// Chunk rows of the partials per layer: ceil(plane / keys) for a single
+// sequence; for a ragged call a bound on the sum of ceil((len[s] + 1) / keys)
+// over sequences that lie inside the planes without overlapping.
+int64_t chunk_rows(int32_t L, int64_t plane, int32_t n_seqs) {
+    return chunk_rows_for(plane, n_seqs, chunk_keys_for(L));
+}
 
 template <int NW, bool RAG>
 hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
@@ -607,15 +610,17 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
     int seqs = 1;
     if (RAG) {
         a.plane = v.rag.total;
-        a.nc_max = ragged_chunk_rows(v.rag.total, v.rag.n);
+        a.chunk_keys = chunk_keys_for(v.L);
+        a.nc_max = static_cast<int32_t>(chunk_rows(v.L, a.plane, v.rag.n));
         a.n_chunks = a.nc_max;  // grid extent per layer
         seqs = v.rag.n;
     } else {
         a.plane = v.cap;
         a.len = v.len;
         a.next_pos = v.next_pos;
-        a.n_chunks = fused_chunks(static_cast<int64_t>(v.len) + 1);
-        a.nc_max = fused_chunks(v.cap);
+        a.chunk_keys = chunk_keys_for(v.L);
+        a.n_chunks = static_cast<int32_t>((static_cast<int64_t>(v.len) + a.chunk_keys) / a.chunk_keys);
+        a.nc_max = static_cast<int32_t>(chunk_rows(v.L, a.plane, 0));
     }
     hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
     hipError_t e = hipGetLastError();
@@ -640,22 +645,16 @@ size_t vz_decode_hdr_bytes(int32_t L) {
     return kHeaderBytes;
 }
 
-namespace {
-int64_t chunk_rows(int64_t plane, int32_t n_seqs) {
-    return n_seqs > 0 ? ragged_chunk_rows(plane, n_seqs) : fused_chunks(plane);
-}
-}  // namespace
-
 bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t L, int64_t plane, int32_t n_seqs) {
     if (dtype != VZ_BF16 || d != D) return false;
     if (!(Hkv == 1 || Hkv == 2 || Hkv == 4 || Hkv == 8)) return false;
     if (Hq % Hkv != 0 || Hq / Hkv > GMAX) return false;
     // 32-bit chunk-row indexes of the partials (the attend grid is smaller)
-    return static_cast<int64_t>(L) * chunk_rows(plane, n_seqs) * Hq < (int64_t(1) << 31);
+    return static_cast<int64_t>(L) * chunk_rows(L, plane, n_seqs) * Hq < (int64_t(1) << 31);
 }
 
 size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs) {
-    const int64_t rows = chunk_rows(plane, n_seqs);
+    const int64_t rows = chunk_rows(L, plane, n_seqs);
     const int32_t seqs = n_seqs > 0 ? n_seqs : 1;
     return vz_decode_hdr_bytes(L) + static_cast<size_t>(L) * rows * Hq * (sizeof(float2) + sizeof(uint16_t) * (D + CHUNK)) +
            static_cast<size_t>(seqs) * L * Hq * sizeof(float2);
