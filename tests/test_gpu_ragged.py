@@ -494,3 +494,17 @@ def test_batch16_ragged_calls():
             assert np.array_equal(from_dev(new_len_d), lens)
             len_d.copy_(new_len_d)
     assert np.array_equal(lens, np.minimum(n_spans + 32, budgets))
+
+
+def test_ragged_many_sequences():
+    """150 short sequences (the lookup scans 64 sequences per round, so three
+    rounds), lengths 0..300 including 0, 127 and 128: decode against the oracle
+    and the single call, then eviction against the oracle, every sequence."""
+    key = synth.stream_key(41, "many")
+    n = 150
+    lens = synth.uniform_int(key, 0, n, 0, 300).astype(np.int64)
+    lens[:4] = [0, 127, 128, 1]
+    _run_decode_case(synth.DT_BF16, 128, 32, 4, lens.tolist(), L=1, steps=1, seed=41)
+    budgets = np.maximum(lens // 2, 8)
+    cases = [(int(x), int(b), int(x) + 3) for x, b in zip(lens, budgets)]
+    _run_evict_case(synth.DT_BF16, 128, 4, cases, L=1, seed=42)
