@@ -93,6 +93,17 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _expect(t, shape, what: str, dtype=None):
+    """The C entry points cannot see tensor sizes, so the binding checks them:
+    a wrong shape or element type raises here instead of reaching a kernel."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} has dtype {t.dtype}, expected {dtype}")
+
+
 def _stream(stream):
     import torch
     s = torch.cuda.current_stream() if stream is None else stream
@@ -127,9 +138,18 @@ def voxzip_fuse_spans(k_in, v_in, span_off, k_out, v_out, score_out, pos_out,
                       anchor_k=None, anchor_v=None, stream=None) -> None:
     """Stage-1 fusion; k_in/v_in [L][H][T_in][d], k_out/v_out [L][H][cap][d],
     span_off int32 [n+1] on the device."""
+    import torch
     L, H, T_in, d = k_in.shape
     cap = k_out.shape[2]
     n = span_off.numel() - 1
+    _expect(v_in, k_in.shape, "v_in", k_in.dtype)
+    _expect(k_out, (L, H, cap, d), "k_out", k_in.dtype)
+    _expect(v_out, (L, H, cap, d), "v_out", k_in.dtype)
+    _expect(score_out, (L, cap), "score_out", torch.float32)
+    _expect(pos_out, (L, cap), "pos_out", torch.int32)
+    _expect(span_off, (n + 1,), "span_off", torch.int32)
+    _expect(anchor_k, (L, H, n, d), "anchor_k", k_in.dtype)
+    _expect(anchor_v, (L, H, n, d), "anchor_v", k_in.dtype)
     _check(lib().voxzip_fuse_spans(_ptr(k_in), _ptr(v_in), T_in, _ptr(span_off), n,
                                    _ptr(anchor_k), _ptr(anchor_v), _ptr(k_out), _ptr(v_out),
                                    _ptr(score_out), _ptr(pos_out), L, H, d, cap,
@@ -139,8 +159,17 @@ def voxzip_fuse_spans(k_in, v_in, span_off, k_out, v_out, score_out, pos_out,
 def voxzip_decode_attend_score(q, k_new, v_new, k_cache, v_cache, score, pos, out, length, next_pos,
                                gamma, sm_scale=0.0, workspace=None, stream=None) -> None:
     """One decode step over all layers; q/out [L][Hq][d], caches [L][Hkv][cap][d]."""
+    import torch
     L, Hkv, cap, d = k_cache.shape
     Hq = q.shape[1]
+    dt = k_cache.dtype
+    _expect(q, (L, Hq, d), "q", dt)
+    _expect(out, (L, Hq, d), "out", dt)
+    _expect(k_new, (L, Hkv, d), "k_new", dt)
+    _expect(v_new, (L, Hkv, d), "v_new", dt)
+    _expect(v_cache, k_cache.shape, "v_cache", dt)
+    _expect(score, (L, cap), "score", torch.float32)
+    _expect(pos, (L, cap), "pos", torch.int32)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().voxzip_decode_attend_score(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
                                             _ptr(v_cache), _ptr(score), _ptr(pos), _ptr(out),
@@ -152,7 +181,12 @@ def voxzip_decode_attend_score(q, k_new, v_new, k_cache, v_cache, score, pos, ou
 def voxzip_evict_compact(k_cache, v_cache, score, pos, length, budget, next_pos, n_sink=4, n_recent=-1,
                          kept_pos_out=None, workspace=None, stream=None) -> int:
     """Stage-2 eviction in place; returns the new resident length."""
+    import torch
     L, Hkv, cap, d = k_cache.shape
+    _expect(v_cache, k_cache.shape, "v_cache", k_cache.dtype)
+    _expect(score, (L, cap), "score", torch.float32)
+    _expect(pos, (L, cap), "pos", torch.int32)
+    _expect(kept_pos_out, (L, int(budget)), "kept_pos_out", torch.int32)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     new_len = ctypes.c_int32(0)
     _check(lib().voxzip_evict_compact(_ptr(k_cache), _ptr(v_cache), _ptr(score), _ptr(pos), int(length),
@@ -200,9 +234,19 @@ def voxzip_fuse_spans_ragged(k_in, v_in, in_base, T_in, span_off, off_base, n_sp
                              anchor_k=None, anchor_v=None, stream=None) -> None:
     """Stage-1 fusion of every sequence of a ragged batch; k_in/v_in
     [L][H][total_in][d], span_off int32 [total_off], outputs [L][H][total][d]."""
+    import torch
     L, H, total_in, d = k_in.shape
     total = k_out.shape[2]
     n = seq_base.numel()
+    _expect(v_in, k_in.shape, "v_in", k_in.dtype)
+    _expect(k_out, (L, H, total, d), "k_out", k_in.dtype)
+    _expect(v_out, (L, H, total, d), "v_out", k_in.dtype)
+    _expect(score_out, (L, total), "score_out", torch.float32)
+    _expect(pos_out, (L, total), "pos_out", torch.int32)
+    if span_off.dtype != torch.int32 or span_off.dim() != 1:
+        raise TypeError("span_off must be a 1-D int32 tensor")
+    _expect(anchor_k, (L, H, total, d), "anchor_k", k_in.dtype)
+    _expect(anchor_v, (L, H, total, d), "anchor_v", k_in.dtype)
     _check(lib().voxzip_fuse_spans_ragged(
         _ptr(k_in), _ptr(v_in), _seq_array(in_base, n, "int64", "in_base"), _seq_array(T_in, n, "int32", "T_in"),
         total_in, _ptr(span_off), _seq_array(off_base, n, "int64", "off_base"),
@@ -219,8 +263,17 @@ def voxzip_decode_attend_score_ragged(q, k_new, v_new, k_cache, v_cache, score, 
     """One decode step of every sequence of a ragged batch; q/out [S][L][Hq][d],
     k_new/v_new [S][L][Hkv][d], caches [L][Hkv][total][d]; length and next_pos
     int32 [S] on the device (not advanced here)."""
+    import torch
     L, Hkv, total, d = k_cache.shape
     n, Hq = q.shape[0], q.shape[2]
+    dt = k_cache.dtype
+    _expect(q, (n, L, Hq, d), "q", dt)
+    _expect(out, (n, L, Hq, d), "out", dt)
+    _expect(k_new, (n, L, Hkv, d), "k_new", dt)
+    _expect(v_new, (n, L, Hkv, d), "v_new", dt)
+    _expect(v_cache, k_cache.shape, "v_cache", dt)
+    _expect(score, (L, total), "score", torch.float32)
+    _expect(pos, (L, total), "pos", torch.int32)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().voxzip_decode_attend_score_ragged(
         _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(score), _ptr(pos), _ptr(out),
@@ -236,8 +289,13 @@ def voxzip_evict_compact_ragged(k_cache, v_cache, score, pos, seq_base, cap, len
                                 workspace=None, stream=None) -> None:
     """Stage-2 eviction of every sequence of a ragged batch, in place;
     new_len_out (int32 [S], device) receives min(length, budget)."""
+    import torch
     L, Hkv, total, d = k_cache.shape
     n = seq_base.numel()
+    _expect(v_cache, k_cache.shape, "v_cache", k_cache.dtype)
+    _expect(score, (L, total), "score", torch.float32)
+    _expect(pos, (L, total), "pos", torch.int32)
+    _expect(kept_pos_out, (L, total), "kept_pos_out", torch.int32)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().voxzip_evict_compact_ragged(
         _ptr(k_cache), _ptr(v_cache), _ptr(score), _ptr(pos), _seq_array(seq_base, n, "int64", "seq_base"),

@@ -232,3 +232,20 @@ def test_ragged_workspace_sizes():
     assert L.voxzip_workspace_bytes_ragged(vz.VZ_OP_DECODE, 48, 32, 4, 128, 80000, 0) == 0
     assert L.voxzip_workspace_bytes_ragged(vz.VZ_OP_DECODE, 48, 32, 4, 128, 1 << 27, 4) == 0
     assert L.voxzip_workspace_bytes_ragged(7, 48, 32, 4, 128, 80000, 16) == 0
+
+
+def test_binding_checks_shapes_before_any_launch():
+    # wrong shapes never reach the library (no GPU needed: the check comes first)
+    torch = pytest.importorskip("torch")
+
+    class Meta:  # a tensor stand-in with a shape and a dtype only
+        def __init__(self, shape, dtype):
+            self.shape, self.dtype = shape, dtype
+
+    bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+    with pytest.raises(ValueError, match="q has shape"):
+        vz._expect(Meta((3, 32, 128), bf), (2, 32, 128), "q", bf)
+    with pytest.raises(TypeError, match="score has dtype"):
+        vz._expect(Meta((2, 64), i32), (2, 64), "score", f32)
+    vz._expect(Meta((2, 64), f32), (2, 64), "score", f32)
+    vz._expect(None, (2, 64), "kept_pos_out", i32)
