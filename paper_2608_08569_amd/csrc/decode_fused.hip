@@ -127,7 +127,8 @@ __device__ __forceinline__ float f16_to_f32(uint16_t x) {
 
 // Kernel arguments shared by the three launches.  A single-sequence call
 // has rag.n == 0 and takes len, next_pos and n_chunks from here; a ragged
-// call reads them per sequence.
+// call reads them per sequence, and n_chunks is then its grid extent per
+// layer (nc_max).
 struct FusedArgs {
     const uint16_t* q;
     const uint16_t* k_new;
@@ -141,7 +142,6 @@ struct FusedArgs {
     int32_t len, next_pos;  // single sequence
     int32_t n_chunks;       // single sequence
     int32_t nc_max;         // chunk rows of the partials per layer (grid bound for a ragged call)
-    int32_t chunk_keys;     // keys per chunk, at most (CHUNK, or fewer for calls with few chunks)
     int32_t Hq, L, hdr_bytes;
     int64_t plane;          // slots per (layer, KV head) plane
     float scale_log2, gamma;
@@ -149,8 +149,8 @@ struct FusedArgs {
 };
 
 // Chunks of sequence s in a ragged call (0 when it cannot be served).
-__device__ __forceinline__ int ragged_chunks(const VzRagged& r, int s, int chunk_keys) {
-    return vz::ragged_decode_status(r, s) == VZ_OK ? (r.len[s] + chunk_keys) / chunk_keys : 0;
+__device__ __forceinline__ int ragged_chunks(const VzRagged& r, int s) {
+    return vz::ragged_decode_status(r, s) == VZ_OK ? (r.len[s] + CHUNK) / CHUNK : 0;
 }
 
 // The sequence a work item belongs to, resolved at the top of every kernel.
@@ -167,7 +167,7 @@ template <bool RAG>
 __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem& it, int& c) {
     if constexpr (RAG) {
         int first = 0, nc = 0;
-        const int s = vz::ragged_locate(f, a.rag.n, a.nc_max, [&](int t) { return ragged_chunks(a.rag, t, a.chunk_keys); },
+        const int s = vz::ragged_locate(f, a.rag.n, a.nc_max, [&](int t) { return ragged_chunks(a.rag, t); },
                                         first, nc);
         if (s < 0 || first + nc > a.nc_max) return false;
         it.s = s;
@@ -518,8 +518,8 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedA
     if constexpr (RAG) {
         s = blockIdx.z;
         const int st = vz::ragged_decode_status(a.rag, s);
-        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u, a.chunk_keys); }) : -1;
-        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s, a.chunk_keys) : 0;
+        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
+        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
         const bool ok = st == VZ_OK && first >= 0 && first + n_chunks <= a.nc_max;
         if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[s] = ok ? VZ_OK : (st != VZ_OK ? st : VZ_ERR_CAPACITY);
         if (!ok) return;
@@ -574,19 +574,12 @@ __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
     if (t < nk) *sc = fmaf(a.gamma, a_old, acc);
 }
 
-// Keys per chunk.  Smaller chunks for calls over few layers were measured and
-// do not help: a one-layer call is bound by its chain of dependent round
-// trips, not by the number of workgroups, and more chunks make the merge
-// heavier.
-int32_t chunk_keys_for(int32_t /*L*/) { return CHUNK; }
-int64_t chunk_rows_for(int64_t plane, int32_t n_seqs, int32_t ck) {
-    return (plane + ck - 1) / ck + (n_seqs > 0 ? n_seqs : 0);
-}
-// Chunk rows of the partials per layer: ceil(plane / keys) for a single
-// sequence; for a ragged call a bound on the sum of ceil((len[s] + 1) / keys)
-// over sequences that lie inside the planes without overlapping.
-int64_t chunk_rows(int32_t L, int64_t plane, int32_t n_seqs) {
-    return chunk_rows_for(plane, n_seqs, chunk_keys_for(L));
+// Chunk rows of the partials per layer: ceil(plane / CHUNK) for a single
+// sequence; for a ragged call ceil(plane / CHUNK) + n_seqs, a bound on the
+// sum of ceil((len[s] + 1) / CHUNK) over sequences that lie inside the planes
+// without overlapping.
+int64_t chunk_rows(int64_t plane, int32_t n_seqs) {
+    return (plane + CHUNK - 1) / CHUNK + (n_seqs > 0 ? n_seqs : 0);
 }
 
 template <int NW, bool RAG>
@@ -610,17 +603,15 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
     int seqs = 1;
     if (RAG) {
         a.plane = v.rag.total;
-        a.chunk_keys = chunk_keys_for(v.L);
-        a.nc_max = static_cast<int32_t>(chunk_rows(v.L, a.plane, v.rag.n));
+        a.nc_max = static_cast<int32_t>(chunk_rows(a.plane, v.rag.n));
         a.n_chunks = a.nc_max;  // grid extent per layer
         seqs = v.rag.n;
     } else {
         a.plane = v.cap;
         a.len = v.len;
         a.next_pos = v.next_pos;
-        a.chunk_keys = chunk_keys_for(v.L);
-        a.n_chunks = static_cast<int32_t>((static_cast<int64_t>(v.len) + a.chunk_keys) / a.chunk_keys);
-        a.nc_max = static_cast<int32_t>(chunk_rows(v.L, a.plane, 0));
+        a.n_chunks = static_cast<int32_t>((static_cast<int64_t>(v.len) + CHUNK) / CHUNK);  // of len + 1 keys
+        a.nc_max = static_cast<int32_t>(chunk_rows(a.plane, 0));
     }
     hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
     hipError_t e = hipGetLastError();
@@ -650,11 +641,11 @@ bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32
     if (!(Hkv == 1 || Hkv == 2 || Hkv == 4 || Hkv == 8)) return false;
     if (Hq % Hkv != 0 || Hq / Hkv > GMAX) return false;
     // 32-bit chunk-row indexes of the partials (the attend grid is smaller)
-    return static_cast<int64_t>(L) * chunk_rows(L, plane, n_seqs) * Hq < (int64_t(1) << 31);
+    return static_cast<int64_t>(L) * chunk_rows(plane, n_seqs) * Hq < (int64_t(1) << 31);
 }
 
 size_t vz_decode_fused_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs) {
-    const int64_t rows = chunk_rows(L, plane, n_seqs);
+    const int64_t rows = chunk_rows(plane, n_seqs);
     const int32_t seqs = n_seqs > 0 ? n_seqs : 1;
     return vz_decode_hdr_bytes(L) + static_cast<size_t>(L) * rows * Hq * (sizeof(float2) + sizeof(uint16_t) * (D + CHUNK)) +
            static_cast<size_t>(seqs) * L * Hq * sizeof(float2);

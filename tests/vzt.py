@@ -112,8 +112,8 @@ class GpuCache:
         return self.dtype == synth.DT_BF16 and self.d == 128 and self.Hkv in (1, 2, 4, 8) and G <= 8
 
     def check_decode_workspace(self):
-        """After every call the decode workspace header is still zero (no
-        kernel flagged an error in it)."""
+        """After every call the decode workspace's reserved header is still
+        zero (no kernel writes outside its partial-result rows)."""
         torch().cuda.synchronize()
         hdr = from_dev(self.ws_dec[:256]).view(np.uint32)
         assert not hdr.any(), f"decode workspace header not zero: {hdr[:4]}"
