@@ -236,3 +236,54 @@ def test_batch16_per_sequence_calls():
             if (t + 1) % w.interval == 0 and g.len > w.budget:
                 synced_evict(g, ref_s, state, w.budget)
         assert g.len == min(n + 32, w.budget)
+
+
+def test_concurrent_calls_on_separate_streams():
+    """Eight sequences decode at the same time, each on its own stream and
+    workspace, with no synchronisation between the calls: no kernel of the
+    library waits for another workgroup, so concurrent kernels cannot starve
+    each other.  Every sequence is checked against the oracle after 3 steps."""
+    import torch
+    L, Hq, Hkv, d, dtype = 4, 32, 4, 128, synth.DT_BF16
+    lens = [6000, 3000, 9000, 257, 8000, 1200, 7000, 4500]
+    caches, refs, streams = [], [], []
+    for i, n in enumerate(lens):
+        k, v, s, p = synth.random_state(60 + i, L, Hkv, d, n + 4, n, dtype, next_pos=n + 7)
+        g = GpuCache(L, Hq, Hkv, d, n + 4, dtype)
+        g.load(k, v, s, p, n, n + 7)
+        caches.append(g)
+        refs.append([k, v, s.astype(np.float64), p])
+        streams.append(torch.cuda.Stream())
+    torch.cuda.synchronize()
+    steps = []
+    for t in range(3):
+        key = synth.stream_key(61, "concurrent", t)
+        mk = lambda tag, shape: synth.as_storage(
+            synth.normal_f32(synth.stream_key(key, tag), int(np.prod(shape))).reshape(shape), dtype)
+        steps.append([(mk(f"q{i}", (L, Hq, d)), mk(f"k{i}", (L, Hkv, d)), mk(f"v{i}", (L, Hkv, d)))
+                      for i in range(len(lens))])
+    dev_steps = [[tuple(to_dev(x) for x in trip) for trip in st] for st in steps]
+    torch.cuda.synchronize()
+    import paper_2608_08569_amd as vz
+    for t in range(3):
+        for i, g in enumerate(caches):  # all sequences' calls in flight together
+            q, kn, vn = dev_steps[t][i]
+            vz.voxzip_decode_attend_score(q, kn, vn, g.k, g.v, g.score, g.pos, g.out, g.len, g.next_pos, 0.95,
+                                          workspace=g.ws_dec, stream=streams[i])
+            g.len += 1
+            g.next_pos += 1
+    torch.cuda.synchronize()
+    for i, g in enumerate(caches):
+        k, v, s, p = refs[i]
+        n = lens[i]
+        K, V = k.copy(), v.copy()
+        S, P = s.copy(), p.copy()
+        for t in range(3):  # the oracle steps from its own state (no eviction: lengths only grow)
+            q, kn, vn = steps[t][i]
+            ro, rs, rp, _ = oracle.decode_step(q, kn, vn, K, V, S, P, n + t, n + 7 + t, 0.95, dtype)
+            K[:, :, n + t], V[:, :, n + t] = kn, vn
+            S[:, : n + t + 1] = rs
+            P[:, : n + t + 1] = rp
+        check_close(widen(from_dev(g.out), dtype), ro, RTOL[dtype], f"sequence {i} output")
+        check_close(from_dev(g.score)[:, : n + 3], S[:, : n + 3], RTOL[dtype], f"sequence {i} score")
+        assert np.array_equal(from_dev(g.pos)[:, : n + 3], P[:, : n + 3])
