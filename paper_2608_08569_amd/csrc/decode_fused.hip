@@ -92,10 +92,10 @@ struct PartialsT {
 using Partials = PartialsT<uint8_t>;
 using ConstPartials = PartialsT<const uint8_t>;
 
-// First key of chunk c of T keys split into n near-equal chunks.
-__host__ __device__ __forceinline__ int chunk_begin(int c, int T, int n) {
-    return static_cast<int>(static_cast<uint64_t>(c) * static_cast<uint64_t>(T) / static_cast<uint64_t>(n));
-}
+// Chunk c of a sequence of T keys: keys [c * CHUNK, min((c + 1) * CHUNK, T)),
+// so every chunk is full except the last (the remainder of T / CHUNK).
+__device__ __forceinline__ int chunk_begin(int c) { return c * CHUNK; }
+__device__ __forceinline__ int chunk_keys(int c, int T) { return min(CHUNK, T - c * CHUNK); }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
     bf16x8_t r;
@@ -205,17 +205,31 @@ __global__ __launch_bounds__(64 * NW, ATTEND_WG_PER_CU) void decode_attend_kerne
     const int g = w;                  // KV head of this wave
 
     Partials part(a.ws, a.hdr_bytes, a.L, nc_max, Hq);
+    // Work order: a single sequence's full chunks of every layer come first
+    // and the layers' short remainder chunks last, so the partial last round
+    // of workgroups is the cheap one.  A ragged call goes layer by layer.
     const int item = blockIdx.x;
-    const int per_layer = RAG ? nc_max : a.n_chunks;
-    const int l = item / per_layer;
+    int l, f;
+    if constexpr (RAG) {
+        l = item / nc_max;
+        f = item - l * nc_max;
+    } else {
+        const int n_full = (a.len + 1) / CHUNK;
+        if (item < a.L * n_full) {
+            l = item / n_full;
+            f = item - l * n_full;
+        } else {
+            l = item - a.L * n_full;
+            f = n_full;
+        }
+    }
     SeqItem it;
     int c;
-    if (!resolve_chunk<RAG>(a, item - l * per_layer, it, c)) return;
+    if (!resolve_chunk<RAG>(a, f, it, c)) return;
     const int len = it.len;
     const int T = len + 1;
-    const int n_chunks = it.n_chunks;
-    const int k_begin = chunk_begin(c, T, n_chunks);
-    const int nk = chunk_begin(c + 1, T, n_chunks) - k_begin;
+    const int k_begin = chunk_begin(c);
+    const int nk = chunk_keys(c, T);
     const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base) * D;
     uint16_t* Kh = a.k_cache + head_base;
     uint16_t* Vh = a.v_cache + head_base;
@@ -547,8 +561,8 @@ __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
     if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) return;
     const ConstPartials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
     const int len = it.len, T = len + 1;
-    const int k_begin = chunk_begin(c, T, it.n_chunks);
-    const int nk = chunk_begin(c + 1, T, it.n_chunks) - k_begin;
+    const int k_begin = chunk_begin(c);
+    const int nk = chunk_keys(c, T);
     const int j = k_begin + (t < nk ? t : 0);
     float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
     const float a_ld = *sc;
