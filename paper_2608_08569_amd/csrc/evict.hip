@@ -22,6 +22,7 @@
 // the selection, the classification and the move lists all stay in LDS: the
 // only other global round trip is the moved rows themselves.
 #include <algorithm>
+#include <type_traits>
 
 #include "vz_internal.h"
 
@@ -48,7 +49,8 @@ struct SelShared {
     uint64_t prefix;
     int krem;
     int cnt;
-    int32_t ev[kSmallE];  // slots of the evicted keys found by the rounds (keys in LDS only)
+    int32_t ev[kSmallE];     // slots of the evicted keys found by the rounds (keys in LDS only)
+    int32_t holes[kSmallE];  // those below the budget, ascending
     int nm;
     int32_t src[kInlineRows], dst[kInlineRows];  // move lists (keys in LDS only)
     uint64_t keys[KEYS ? kLdsSlots : 1];
@@ -148,24 +150,32 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh)
     const int32_t recent_from = next_pos - M;
     auto is_mid = [&](int32_t p) { return p >= n_sink && p < recent_from; };
     if (LK) {
-        // 8 slots per thread and round, every load issued before any use (no
-        // load behind a branch)
-        constexpr int B = 8;
-        for (int j0 = tid; j0 < len; j0 += B * kSel) {
+        // Every slot's key in one round: up to kLdsSlots / kSel slots per
+        // thread, all loads issued before any use (indexes past the end are
+        // clamped, so no load sits behind a branch).  8 per thread while they
+        // suffice, 16 otherwise (e.g. 8193 slots would take a second round
+        // trip at 8).
+        auto load_keys = [&](auto per_thread) {
+            constexpr int B = decltype(per_thread)::value;
             int32_t pv[B];
             float av[B];
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const int j = min(j0 + b * kSel, len - 1);
+                const int j = min(tid + b * kSel, len - 1);
                 pv[b] = P[j];
                 av[b] = A[j];
             }
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const int j = j0 + b * kSel;
+                const int j = tid + b * kSel;
                 if (j < len) s_keys[j] = is_mid(pv[b]) ? vz::rank_key(av[b], pv[b]) : kNoKey;
             }
-        }
+        };
+        static_assert(kLdsSlots == 16 * kSel, "one round of 16 keys per thread covers the LDS key array");
+        if (len <= 8 * kSel)
+            load_keys(std::integral_constant<int, 8>{});
+        else
+            load_keys(std::integral_constant<int, 16>{});
         __syncthreads();
     }
     // key of slot j and whether it competes
@@ -211,7 +221,8 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh)
             // (at most kSmallE of each, so one thread pairs them).
             __syncthreads();
             if (tid == 0) {
-                int holes[kSmallE], nh = 0;
+                int32_t* const holes = sh.holes;  // in LDS: indexed at run time without scratch memory
+                int nh = 0;
                 for (int r = 0; r < found; ++r)
                     if (s_ev[r] < budget) holes[nh++] = s_ev[r];
                 for (int a = 1; a < nh; ++a)  // ascending slots
