@@ -19,6 +19,13 @@ FLAGS = [
 ]
 
 
+# per-source extra flags: the whole-range decode kernel needs the max-ILP
+# machine scheduler to fit its 256 registers per lane without spilling
+FILE_FLAGS = {
+    "decode_range.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+}
+
+
 def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
@@ -31,7 +38,8 @@ def build(out: str = LIB, verbose: bool = False, extra: tuple = ()) -> str:
     procs = []
     for src in sources():
         obj = os.path.join(build_dir, os.path.basename(src) + ".o")
-        cmd = [HIPCC, *[f for f in FLAGS if f != "-shared"], *extra, "-c", src, "-o", obj]
+        cmd = [HIPCC, *[f for f in FLAGS if f != "-shared"], *FILE_FLAGS.get(os.path.basename(src), []), *extra,
+               "-c", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True), src))

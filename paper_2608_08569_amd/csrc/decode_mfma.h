@@ -1,0 +1,116 @@
+// Definitions shared by the MFMA decode kernels (bfloat16 caches, d = 128,
+// at most 8 query heads per KV head): tile geometry, operand helpers and the
+// kernel arguments.  Included by the chunked path (decode_fused.hip) and the
+// whole-range path (decode_range.hip).
+#pragma once
+
+#include <math.h>
+
+#include "vz_internal.h"
+
+namespace vz_mfma {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int D = 128;
+constexpr int GMAX = 8;                // query heads per KV head served here
+constexpr int TILES = 8;               // 16-key MFMA tiles per chunk
+constexpr int PAIRS = TILES / 2;       // packed tile pairs = 32-key tiles
+constexpr int CHUNK = 16 * TILES;      // keys per chunk (at most)
+constexpr int VT = 32;                 // keys per staged tile
+constexpr int KSTEPS = D / 32;         // MFMA k-steps over the channels
+constexpr int DTILES = D / 16;         // output column tiles
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kRor8 = 0x128;           // DPP row_ror:8 (swap the halves of each 16-lane row)
+constexpr int kBufferDword3 = 0x00020000;  // raw buffer descriptor word 3 (32-bit data format)
+
+// Staged tiles are 32 rows of 256 bytes with padded row strides, so that every
+// LDS address is one per-lane base plus an immediate (bank analysis in the
+// design notes): K rows 272 bytes apart (16 rows at one 16-byte column fall on
+// 16 distinct bank groups), V rows 288 bytes apart (4 rows x 32 bytes of a
+// transposed read fall on distinct banks).
+constexpr int KSTRIDE = 256 + 16;
+constexpr int VSTRIDE = 256 + 32;
+constexpr int TILE_BYTES = VT * VSTRIDE;
+
+// Chunk c of a sequence of T keys: keys [c * CHUNK, min((c + 1) * CHUNK, T)),
+// so every chunk is full except the last (the remainder of T / CHUNK).
+__device__ __forceinline__ int chunk_begin(int c) { return c * CHUNK; }
+__device__ __forceinline__ int chunk_keys(int c, int T) { return min(CHUNK, T - c * CHUNK); }
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
+    bf16x8_t r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+
+__device__ __forceinline__ float ror8(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kRor8, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return static_cast<uint32_t>(vz::f32_to_bf16(a)) | (static_cast<uint32_t>(vz::f32_to_bf16(b)) << 16);
+}
+
+// Sum over the 8 lanes of a half row (lanes 0..7 and 8..15 of every 16-lane
+// row), complete in lanes 0..3 and 8..11: DPP swaps within quads, then a
+// row rotate brings in the neighbouring quad (row_ror:12, lane i reading lane
+// i + 4 of its row).
+constexpr int kQuadXor1 = 0xB1;  // quad_perm [1, 0, 3, 2]
+constexpr int kQuadXor2 = 0x4E;  // quad_perm [2, 3, 0, 1]
+constexpr int kRor12 = 0x12C;    // row_ror:12
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float sum_heads8(float v) {
+    v += dpp<kQuadXor1>(v);
+    v += dpp<kQuadXor2>(v);
+    return v + dpp<kRor12>(v);
+}
+
+// Half precision (round to nearest even) pack / unpack.
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+    const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
+    uint16_t ua, ub;
+    __builtin_memcpy(&ua, &ha, 2);
+    __builtin_memcpy(&ub, &hb, 2);
+    return static_cast<uint32_t>(ua) | (static_cast<uint32_t>(ub) << 16);
+}
+__device__ __forceinline__ float f16_to_f32(uint16_t x) {
+    _Float16 h;
+    __builtin_memcpy(&h, &x, 2);
+    return static_cast<float>(h);
+}
+
+// Kernel arguments shared by the decode launches.  A single-sequence call
+// has rag.n == 0 and takes len, next_pos and n_chunks from here; a ragged
+// call reads them per sequence, and n_chunks is then its grid extent per
+// layer (nc_max).
+struct FusedArgs {
+    const uint16_t* q;
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    uint16_t* k_cache;
+    uint16_t* v_cache;
+    int32_t* pos;
+    float* score;
+    uint16_t* out;
+    uint8_t* ws;
+    int32_t len, next_pos;  // single sequence
+    int32_t n_chunks;       // single sequence
+    int32_t nc_max;         // chunk rows of the partials per layer (grid bound for a ragged call)
+    int32_t Hq, L, hdr_bytes;
+    int64_t plane;          // slots per (layer, KV head) plane
+    float scale_log2, gamma;
+    VzRagged rag;
+};
+
+}  // namespace vz_mfma
+
+// Whole-range path (decode_range.hip): whether a single-sequence call of len
+// resident keys over L layers and Hkv KV heads takes it, and its launches.
+bool vz_decode_range_ok(int32_t len, int32_t L, int32_t Hkv);
+hipError_t vz_launch_decode_range(const vz_mfma::FusedArgs& a, int32_t Hkv, hipStream_t stream);

@@ -1,9 +1,10 @@
 """GPU parity of the whole-range decode path: single-sequence bf16 calls with at
-least 128 (layer, KV head) items and at most 9216 keys, where one workgroup
+least 128 (layer, KV head) items and at most 8224 keys, where one workgroup
 streams every key of a (layer, KV head).  State-synced against the fp64 oracle
 (every layer for short caches, sampled layers for long ones); the cases cover
-caches shorter than one chunk per wave, ragged tails, the 9216-key maximum and
-the first length past it (chunked path), 1 to 8 query heads per KV head."""
+caches shorter than one chunk per wave, ragged tails, the 8224-key maximum
+(8 chunks per wave and one 32-key tile) and the first length past it (chunked
+path), 1 to 8 query heads per KV head."""
 import numpy as np
 import pytest
 
@@ -59,10 +60,11 @@ def test_whole_range_short_all_layers(length):
     run_case(32, 4, 32, length, steps=2)
 
 
-@pytest.mark.parametrize("length", [4095, 8192, 9214, 9215, 9216])
+@pytest.mark.parametrize("length", [4095, 8191, 8192, 8222, 8223, 8224])
 def test_whole_range_long_sampled_layers(length):
-    """Up to 9 chunks per wave (9215 -> 9216 keys, the whole-range maximum)
-    and the first cache past it (chunked path); layers 0, 13 and 31."""
+    """8 full chunks per wave (8191 -> 8192 keys), one more key or tile on
+    the last wave (up to 8223 -> 8224 keys, the whole-range maximum) and the
+    first cache past it (chunked path); layers 0, 13 and 31."""
     run_case(32, 4, 32, length, steps=1, layers=[0, 13, 31])
 
 
