@@ -37,7 +37,7 @@ import synth  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 PROFILE_PMC = os.path.join(ROOT, "profiles", "decode_long32k_pmc.md")
 KERNEL_SRC = [os.path.join(ROOT, "paper_2608_08569_amd", "csrc", f)
-              for f in ("decode_fused.hip", "decode_generic.hip")]
+              for f in ("decode_range.hip", "decode_mfma.h", "decode_fused.hip", "decode_generic.hip")]
 
 
 def log(*a):
@@ -569,8 +569,8 @@ def main():
         "fuse_ms_mean": float(np.mean(fuse_ms)),
         "fuse_gbps": fuse_bytes / (float(np.mean(fuse_ms)) * 1e-3) / 1e9,
         "roofline": {
-            "kernel": ("voxzip_decode_attend_score = decode_attend_kernel + decode_output_kernel + "
-                       "decode_fold_kernel (48 layers, T=8193)"),
+            "kernel": ("voxzip_decode_attend_score = decode_range_kernel + decode_range_fold_kernel "
+                       "(whole-range path: one workgroup per layer and KV head; 48 layers, T=8193)"),
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,

@@ -63,7 +63,9 @@ constexpr int kQuadXor2 = 0x4E;  // quad_perm [2, 3, 0, 1]
 constexpr int kRor12 = 0x12C;    // row_ror:12
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+    // every source lane of these patterns exists, so bound_ctrl changes
+    // nothing but lets the move fold into the add (v_add_f32_dpp)
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 __device__ __forceinline__ float sum_heads8(float v) {
     v += dpp<kQuadXor1>(v);

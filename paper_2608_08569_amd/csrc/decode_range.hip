@@ -12,9 +12,12 @@ using namespace vz_mfma;
 // ---- whole-range path: single-sequence calls over many (layer, KV head) items ----
 // One workgroup of RW waves per (layer, KV head) streams every key of the
 // head, so the softmax of its query heads completes inside the workgroup:
-// wave w takes a contiguous run of about n_chunks / RW chunks (contiguous
-// runs stream about 7 % faster than chunks dealt round-robin to the waves)
-// and keeps, per head, a running
+// wave w takes a contiguous run of about 1 / RW of the full 128-key chunks
+// (contiguous runs stream about 7 % faster than chunks dealt round-robin to
+// the waves), and wave 0 also the last, partial chunk: the first wave of each
+// SIMD gets the memory pipe first and finishes tens of microseconds ahead of
+// the second, so work added to it stays off the critical path.  Each wave
+// keeps, per head, a running
 // max, sum and output (online softmax, the output rescaled whenever the max
 // grows), plus each chunk's p~ = exp2(s - m_ref) in half precision (the
 // first RLDS chunks in LDS, the others in registers) and the reference max
@@ -52,16 +55,23 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     const int Hq = a.Hq, G = Hq / NW;
     const int g = blockIdx.x, l = blockIdx.y;
     const int len = a.len, T = len + 1;
-    const int n_chunks = (T + CHUNK - 1) / CHUNK;
-    const int c0 = __builtin_amdgcn_readfirstlane(w * n_chunks / RW);  // the wave's chunks: [c0, c0 + my_chunks)
-    const int my_chunks = __builtin_amdgcn_readfirstlane((w + 1) * n_chunks / RW - c0);
+    const int n_full = T / CHUNK;            // full chunks; chunk n_full holds the other T % CHUNK keys
+    const bool part = T % CHUNK != 0;
+    const int c0 = __builtin_amdgcn_readfirstlane(w * n_full / RW);  // the wave's full chunks: [c0, c0 + my_full)
+    const int my_full = __builtin_amdgcn_readfirstlane((w + 1) * n_full / RW - c0);
+    const int my_chunks = my_full + (w == 0 && part ? 1 : 0);
+    // Chunk of the wave's slot k.  Wave 0 has the fewest full chunks
+    // (n_full / RW), so the partial chunk is at most its slot RFULL, and there
+    // only when n_full = RW * RFULL, where the host limit leaves it <= VT keys.
+    auto chunk_of = [&](int k) { return k < my_full ? c0 + k : n_full; };
     const size_t head_base = (static_cast<size_t>(l) * NW + g) * a.plane * D;
     uint16_t* Kh = a.k_cache + head_base;
     uint16_t* Vh = a.v_cache + head_base;
 
-    // Eq. (1) first: the last wave, whose chunks hold slot len, writes the new
-    // row before any of its loads, so every key is read from the cache alike.
-    if (w == RW - 1) {
+    // Eq. (1) first: the wave whose chunks hold slot len (the partial chunk's
+    // wave 0, else the last wave) writes the new row before any of its loads,
+    // so every key is read from the cache alike.
+    if (w == (part ? 0 : RW - 1)) {
         const uint16_t* kn = a.k_new + (static_cast<size_t>(l) * NW + g) * D;
         const uint16_t* vn = a.v_new + (static_cast<size_t>(l) * NW + g) * D;
         if (lane < 16)
@@ -74,7 +84,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         __threadfence_block();
     }
 
-    // Tile t of the wave (t = 8 k + j): chunk c0 + k, K tiles j = 0..3 and
+    // Tile t of the wave (t = 8 k + j): chunk chunk_of(k), K tiles j = 0..3 and
     // V tiles j = 4..7, 32 rows each.  Two tiles are in flight, in register
     // sets t & 1.  A tile past the wave's chunks has an empty descriptor: its
     // loads return zero and touch no memory.
@@ -82,7 +92,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     uint4 stg[2][8];
     auto load_tile = [&](int k, int j, uint4 (&dst)[8]) {
         const bool live = k < my_chunks;
-        const int c = live ? c0 + k : 0;
+        const int c = live ? chunk_of(k) : 0;
         const int nk = live ? min(CHUNK, T - c * CHUNK) : 0;
         const int u = j & 3;
         const int rows = nk - VT * u > 0 ? nk - VT * u : 0;
@@ -130,7 +140,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
 #pragma unroll
     for (int k = 0; k < RNCH; ++k) {
         if (k < my_chunks) {
-        const int c = c0 + k;
+        const int c = chunk_of(k);
         const int nk = min(CHUNK, T - c * CHUNK);
         // ---- pass 1: logits S^T = K Q^T ----
         float sp[PAIRS][4];
@@ -272,11 +282,15 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     // ---- each key's sum over this KV head's query heads of p_hj ----
     float* const gsum = reinterpret_cast<float*>(a.ws + a.hdr_bytes) + (static_cast<size_t>(l) * NW + g) * range_row(a.plane);
     const float fh = hh < G ? inv_S : 0.f;
+    // Every slot is computed without a branch (slots past the wave's chunks
+    // hold stale values and are not stored), so the nine chunks' latency
+    // chains overlap instead of running one after another.
 #pragma unroll
     for (int k = 0; k < RNCH; ++k) {
-        if (k < my_chunks) {
+        {
+        const bool live = k < my_chunks;
         const float f = exp2f(s_mref[w][k][hh] - M) * fh;
-        float* const dst = gsum + (c0 + k) * CHUNK + 16 * hi + 4 * q4;
+        float* const dst = gsum + (live ? chunk_of(k) : 0) * CHUNK + 16 * hi + 4 * q4;
         uint32_t pk[2 * PAIRS];
         if (k < RLDS) {
             const uint4 p0 = s_pst[w][k][0][lane], p1 = s_pst[w][k][1][lane];
@@ -300,7 +314,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
             x[3] = f16_to_f32(static_cast<uint16_t>(pk[2 * u + 1] >> 16)) * f;
 #pragma unroll
             for (int i = 0; i < 4; ++i) x[i] = sum_heads8(x[i]);
-            if (hh == 0) *reinterpret_cast<float4*>(dst + VT * u) = make_float4(x[0], x[1], x[2], x[3]);
+            if (hh == 0 && live) *reinterpret_cast<float4*>(dst + VT * u) = make_float4(x[0], x[1], x[2], x[3]);
         }
         }
     }
