@@ -54,25 +54,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
     return static_cast<uint32_t>(vz::f32_to_bf16(a)) | (static_cast<uint32_t>(vz::f32_to_bf16(b)) << 16);
 }
 
-// Sum over the 8 lanes of a half row (lanes 0..7 and 8..15 of every 16-lane
-// row), complete in lanes 0..3 and 8..11: DPP swaps within quads, then a
-// row rotate brings in the neighbouring quad (row_ror:12, lane i reading lane
-// i + 4 of its row).
-constexpr int kQuadXor1 = 0xB1;  // quad_perm [1, 0, 3, 2]
-constexpr int kQuadXor2 = 0x4E;  // quad_perm [2, 3, 0, 1]
-constexpr int kRor12 = 0x12C;    // row_ror:12
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    // every source lane of these patterns exists, so bound_ctrl changes
-    // nothing but lets the move fold into the add (v_add_f32_dpp)
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
-}
-__device__ __forceinline__ float sum_heads8(float v) {
-    v += dpp<kQuadXor1>(v);
-    v += dpp<kQuadXor2>(v);
-    return v + dpp<kRor12>(v);
-}
-
 // Half precision (round to nearest even) pack / unpack.
 __device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
     const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);

@@ -280,25 +280,26 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     }
 
     // ---- each key's sum over this KV head's query heads of p_hj ----
+    // Per chunk, each lane scales its values (one head, 16 keys) and writes
+    // them to the wave's LDS scratch as [key][head] rows; each lane then reads
+    // two keys' rows back and adds them.  The key slots are XOR-swizzled so
+    // that the 8 keys of one write instruction fall on 8 distinct bank groups.
+    // (LDS operations of a wave complete in order, so the wave needs no
+    // barrier between its own writes and reads.)
+    __syncthreads();  // the output merge has read the tile buffers
+    static_assert(CHUNK * GMAX * 4 <= TILE_BYTES, "a chunk's rows fit in the wave's tile buffer");
+    float* const xs = reinterpret_cast<float*>(s_tile[w]);  // [CHUNK][GMAX] floats of this wave
+    auto slot = [](int r) { return r ^ ((r >> 3) & 3); };
     float* const gsum = reinterpret_cast<float*>(a.ws + a.hdr_bytes) + (static_cast<size_t>(l) * NW + g) * range_row(a.plane);
     const float fh = hh < G ? inv_S : 0.f;
-    // Every slot is computed without a branch (slots past the wave's chunks
-    // hold stale values and are not stored), so the nine chunks' latency
-    // chains overlap instead of running one after another.
-#pragma unroll
-    for (int k = 0; k < RNCH; ++k) {
-        {
-        const bool live = k < my_chunks;
+#pragma unroll 1
+    for (int k = 0; k < my_chunks; ++k) {
         const float f = exp2f(s_mref[w][k][hh] - M) * fh;
-        float* const dst = gsum + (live ? chunk_of(k) : 0) * CHUNK + 16 * hi + 4 * q4;
         uint32_t pk[2 * PAIRS];
         if (k < RLDS) {
             const uint4 p0 = s_pst[w][k][0][lane], p1 = s_pst[w][k][1][lane];
             pk[0] = p0.x, pk[1] = p0.y, pk[2] = p0.z, pk[3] = p0.w;
             pk[4] = p1.x, pk[5] = p1.y, pk[6] = p1.z, pk[7] = p1.w;
-        } else if (k < RFULL) {
-#pragma unroll
-            for (int i = 0; i < 2 * PAIRS; ++i) pk[i] = pst[k - RLDS][i];
         } else {
             pk[0] = pst_last[0];
             pk[1] = pst_last[1];
@@ -306,17 +307,27 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
             for (int i = 2; i < 2 * PAIRS; ++i) pk[i] = 0;  // keys past the cache: p~ = 0
         }
 #pragma unroll
-        for (int u = 0; u < PAIRS; ++u) {
-            float x[4];
-            x[0] = f16_to_f32(static_cast<uint16_t>(pk[2 * u] & 0xffffu)) * f;
-            x[1] = f16_to_f32(static_cast<uint16_t>(pk[2 * u] >> 16)) * f;
-            x[2] = f16_to_f32(static_cast<uint16_t>(pk[2 * u + 1] & 0xffffu)) * f;
-            x[3] = f16_to_f32(static_cast<uint16_t>(pk[2 * u + 1] >> 16)) * f;
+        for (int r = 0; r < RFULL - RLDS; ++r)  // register slots: fixed indexes, wave-uniform choice
+            if (k == RLDS + r) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) x[i] = sum_heads8(x[i]);
-            if (hh == 0 && live) *reinterpret_cast<float4*>(dst + VT * u) = make_float4(x[0], x[1], x[2], x[3]);
+                for (int i = 0; i < 2 * PAIRS; ++i) pk[i] = pst[r][i];
+            }
+#pragma unroll
+        for (int u = 0; u < PAIRS; ++u)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint16_t h16 = static_cast<uint16_t>(pk[2 * u + (i >> 1)] >> (16 * (i & 1)));
+                const int key = VT * u + 16 * hi + 4 * q4 + i;
+                xs[slot(key) * GMAX + hh] = f16_to_f32(h16) * f;
+            }
+        float y[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const float4* row = reinterpret_cast<const float4*>(xs + slot(2 * lane + e) * GMAX);
+            const float4 a0 = row[0], a1 = row[1];
+            y[e] = ((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w));
         }
-        }
+        *reinterpret_cast<float2*>(gsum + chunk_of(k) * CHUNK + 2 * lane) = make_float2(y[0], y[1]);
     }
 }
 
