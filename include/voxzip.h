@@ -93,6 +93,14 @@ VZ_API int voxzip_build_span_offsets(const int64_t *t_start_ms, const int64_t *t
  *   for every layer l, KV head h and span j < n_spans.
  *
  *  k_in, v_in   [n_layers][kv_heads][T_in][d]  input (prefill) K and V.
+ *               v_in and v_out may both be NULL: then only k is fused (and
+ *               anchor_v must be NULL).  That serves the embedding-space form
+ *               of Sec. 3.2.1 -- the audio-token input embeddings as k_in with
+ *               n_layers = kv_heads = 1 and d = d_model, the text-token
+ *               embeddings of each span as anchor_k (zero rows for
+ *               background spans).
+ *  d            64 or 128 for every dtype; fusion also takes any multiple of
+ *               16 bytes (8 bf16 or 4 float32 elements) up to 16384.
  *  span_off     int32 [n_spans + 1], device.  Groups are contiguous and in
  *               time order: span_off[0] = 0, strictly increasing,
  *               span_off[n_spans] = T_in.  A background token is a span of
@@ -104,8 +112,10 @@ VZ_API int voxzip_build_span_offsets(const int64_t *t_start_ms, const int64_t *t
  *  score_out    float32 [n_layers][cap_out]; pos_out int32 [n_layers][cap_out].
  * Arithmetic: float32 sum in row order, IEEE division by the span length,
  * float32 anchor add, one rounding to dtype (nearest-even).
- * Errors: VZ_ERR_INVALID for null pointers or k_in/v_in aliasing an output,
- * VZ_ERR_CAPACITY if n_spans > cap_out, VZ_ERR_SHAPE if n_spans > T_in.
+ * Errors: VZ_ERR_INVALID for null pointers (other than v_in/v_out together),
+ * k_in/v_in aliasing an output or anchor_v without v_in; VZ_ERR_CAPACITY if
+ * n_spans > cap_out; VZ_ERR_SHAPE if n_spans > T_in; VZ_ERR_UNSUPPORTED for
+ * a row size fusion does not take.
  */
 VZ_API int voxzip_fuse_spans(const void *k_in, const void *v_in, int32_t T_in,
                       const int32_t *span_off, int32_t n_spans,
@@ -224,6 +234,8 @@ VZ_API size_t voxzip_workspace_bytes_ragged(int32_t op, int32_t n_layers, int32_
  *               with more spans gets VZ_ERR_CAPACITY.
  *  anchor_k/v   NULL, or laid out like the outputs (row j of sequence s at
  *               slot seq_base[s] + j).
+ *  v_in, v_out, d  as for voxzip_fuse_spans: v_in and v_out both NULL fuse k
+ *               alone; wide rows (the embedding-space form) are taken.
  *  k_out, v_out, score_out, pos_out  packed outputs; sequence s gets
  *               n_spans[s] rows from slot seq_base[s] (n_spans[s] <= cap[s]),
  *               pos = 0 .. n_spans[s] - 1, score 0.

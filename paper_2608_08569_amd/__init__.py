@@ -137,7 +137,8 @@ def voxzip_workspace_bytes(op: int, n_layers: int, n_q_heads: int, kv_heads: int
 def voxzip_fuse_spans(k_in, v_in, span_off, k_out, v_out, score_out, pos_out,
                       anchor_k=None, anchor_v=None, stream=None) -> None:
     """Stage-1 fusion; k_in/v_in [L][H][T_in][d], k_out/v_out [L][H][cap][d],
-    span_off int32 [n+1] on the device."""
+    span_off int32 [n+1] on the device.  v_in and v_out may both be None (k
+    alone: the embedding-space form, k_in = [1][1][L_a][d_model])."""
     import torch
     L, H, T_in, d = k_in.shape
     cap = k_out.shape[2]

@@ -30,16 +30,40 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
     return pa < pb + nb && pb < pa + na;
 }
 
-int check_common(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtype) {
+// Fusion also takes wide rows (the embedding-space form of Stage 1: one head of
+// width d_model): any multiple of one 16-byte vector up to kFuseMaxD.
+constexpr int32_t kFuseMaxD = 16384;
+
+int check_common(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtype, bool fusion = false) {
     if (L < 1 || Hkv < 1 || d < 1) return fail(VZ_ERR_SHAPE, fn, "sizes must be positive");
     if (dtype != VZ_F32 && dtype != VZ_BF16) return fail(VZ_ERR_UNSUPPORTED, fn, "dtype must be VZ_F32 or VZ_BF16");
-    if (d != 64 && d != 128) return fail(VZ_ERR_UNSUPPORTED, fn, "head size must be 64 or 128");
+    if (fusion) {
+        const int32_t vec = dtype == VZ_F32 ? 4 : 8;  // elements per 16 bytes
+        if (d != 64 && d != 128 && (d % vec != 0 || d > kFuseMaxD))
+            return fail(VZ_ERR_UNSUPPORTED, fn, "row size must be 64, 128 or a multiple of 16 bytes up to 16384");
+    } else if (d != 64 && d != 128) {
+        return fail(VZ_ERR_UNSUPPORTED, fn, "head size must be 64 or 128");
+    }
     if (L > 65535) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 65535 layers");
     return VZ_OK;
 }
 
-int check_ragged(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtype, int64_t total, int32_t n_seqs) {
-    int rc = check_common(fn, L, Hkv, d, dtype);
+// K and V, or K alone (v_in and v_out both NULL; then no anchor_v).
+int check_fuse_pointers(const char* fn, const void* v_in, const void* v_out, const void* anchor_k,
+                        const void* anchor_v) {
+    if ((v_in == nullptr) != (v_out == nullptr))
+        return fail(VZ_ERR_INVALID, fn, "v_in and v_out must both be given or both be NULL");
+    if (v_in == nullptr) {
+        if (anchor_v) return fail(VZ_ERR_INVALID, fn, "anchor_v given without v_in");
+    } else if ((anchor_k == nullptr) != (anchor_v == nullptr)) {
+        return fail(VZ_ERR_INVALID, fn, "anchor_k and anchor_v must both be given or both be NULL");
+    }
+    return VZ_OK;
+}
+
+int check_ragged(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtype, int64_t total, int32_t n_seqs,
+                 bool fusion = false) {
+    int rc = check_common(fn, L, Hkv, d, dtype, fusion);
     if (rc) return rc;
     if (n_seqs < 1 || n_seqs > kRaggedMaxSeqs) return fail(VZ_ERR_SHAPE, fn, "n_seqs must be in [1, 32768]");
     if (total < 1 || total > kRaggedMaxTotal) return fail(VZ_ERR_SHAPE, fn, "total must be in [1, 2^26]");
@@ -110,12 +134,12 @@ int voxzip_fuse_spans(const void* k_in, const void* v_in, int32_t T_in, const in
                       int32_t* pos_out, int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap_out,
                       int32_t dtype, void* stream) {
     static const char* fn = "voxzip_fuse_spans";
-    if (!k_in || !v_in || !span_off || !k_out || !v_out || !score_out || !pos_out)
-        return fail(VZ_ERR_INVALID, fn, "null pointer");
-    if ((anchor_k == nullptr) != (anchor_v == nullptr))
-        return fail(VZ_ERR_INVALID, fn, "anchor_k and anchor_v must both be given or both be NULL");
-    int rc = check_common(fn, n_layers, kv_heads, d, dtype);
+    if (!k_in || !span_off || !k_out || !score_out || !pos_out) return fail(VZ_ERR_INVALID, fn, "null pointer");
+    int rc = check_fuse_pointers(fn, v_in, v_out, anchor_k, anchor_v);
     if (rc) return rc;
+    rc = check_common(fn, n_layers, kv_heads, d, dtype, true);
+    if (rc) return rc;
+    if (2 * static_cast<int64_t>(kv_heads) > 65535) return fail(VZ_ERR_UNSUPPORTED, fn, "too many KV heads");
     if (T_in < 0 || n_spans < 0 || cap_out < 1) return fail(VZ_ERR_SHAPE, fn, "negative size");
     if (n_spans > T_in) return fail(VZ_ERR_SHAPE, fn, "more spans than input tokens");
     if (n_spans > cap_out) return fail(VZ_ERR_CAPACITY, fn, "n_spans exceeds cap_out");
@@ -126,9 +150,10 @@ int voxzip_fuse_spans(const void* k_in, const void* v_in, int32_t T_in, const in
     void* outs[2] = {k_out, v_out};
     for (const void* i : ins)
         for (void* o : outs)
-            if (in_bytes && overlaps(i, in_bytes, o, out_bytes))
+            if (i && o && in_bytes && overlaps(i, in_bytes, o, out_bytes))
                 return fail(VZ_ERR_INVALID, fn, "an input aliases an output");
-    if (overlaps(k_out, out_bytes, v_out, out_bytes)) return fail(VZ_ERR_INVALID, fn, "k_out and v_out overlap");
+    if (v_out && overlaps(k_out, out_bytes, v_out, out_bytes))
+        return fail(VZ_ERR_INVALID, fn, "k_out and v_out overlap");
     hipError_t e = vz_launch_fuse(k_in, v_in, T_in, span_off, n_spans, anchor_k, anchor_v, k_out, v_out, score_out,
                                   pos_out, n_layers, kv_heads, d, cap_out, dtype, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
@@ -197,17 +222,17 @@ int voxzip_fuse_spans_ragged(const void* k_in, const void* v_in, const int64_t* 
                              int32_t* status, int32_t n_layers, int32_t kv_heads, int32_t d, int32_t dtype,
                              void* stream) {
     static const char* fn = "voxzip_fuse_spans_ragged";
-    if (!k_in || !v_in || !in_base || !T_in || !span_off || !off_base || !n_spans || !k_out || !v_out ||
-        !score_out || !pos_out || !seq_base || !cap)
+    if (!k_in || !in_base || !T_in || !span_off || !off_base || !n_spans || !k_out || !score_out || !pos_out ||
+        !seq_base || !cap)
         return fail(VZ_ERR_INVALID, fn, "null pointer");
-    if ((anchor_k == nullptr) != (anchor_v == nullptr))
-        return fail(VZ_ERR_INVALID, fn, "anchor_k and anchor_v must both be given or both be NULL");
-    int rc = check_ragged(fn, n_layers, kv_heads, d, dtype, total, n_seqs);
+    int rc = check_fuse_pointers(fn, v_in, v_out, anchor_k, anchor_v);
+    if (rc) return rc;
+    rc = check_ragged(fn, n_layers, kv_heads, d, dtype, total, n_seqs, true);
     if (rc) return rc;
     if (total_in < 0 || total_off < 1 || max_spans < 0) return fail(VZ_ERR_SHAPE, fn, "negative size");
     if (total_in > kRaggedMaxTotal || max_spans > total) return fail(VZ_ERR_SHAPE, fn, "size out of range");
     if (2 * static_cast<int64_t>(kv_heads) > 65535) return fail(VZ_ERR_UNSUPPORTED, fn, "too many KV heads");
-    if ((static_cast<int64_t>(max_spans) + 15) / 16 * n_seqs >= (int64_t(1) << 31))
+    if (static_cast<int64_t>(max_spans > 0 ? max_spans : 1) * n_seqs >= (int64_t(1) << 31))
         return fail(VZ_ERR_UNSUPPORTED, fn, "max_spans x n_seqs too large");
     const size_t es = elem_size(dtype);
     const size_t in_bytes = static_cast<size_t>(n_layers) * kv_heads * total_in * d * es;
@@ -216,9 +241,10 @@ int voxzip_fuse_spans_ragged(const void* k_in, const void* v_in, const int64_t* 
     void* outs[2] = {k_out, v_out};
     for (const void* i : ins)
         for (void* o : outs)
-            if (in_bytes && overlaps(i, in_bytes, o, out_bytes))
+            if (i && o && in_bytes && overlaps(i, in_bytes, o, out_bytes))
                 return fail(VZ_ERR_INVALID, fn, "an input aliases an output");
-    if (overlaps(k_out, out_bytes, v_out, out_bytes)) return fail(VZ_ERR_INVALID, fn, "k_out and v_out overlap");
+    if (v_out && overlaps(k_out, out_bytes, v_out, out_bytes))
+        return fail(VZ_ERR_INVALID, fn, "k_out and v_out overlap");
     VzFuseRaggedArgs a{k_in,     v_in,     in_base,  T_in,     span_off, off_base,  n_spans,  anchor_k,
                        anchor_v, k_out,    v_out,    score_out, pos_out, seq_base,  cap,      status,
                        n_seqs,   total_in, total_off, total,   max_spans, n_layers, kv_heads, d,

@@ -1,5 +1,9 @@
 // Stage-1 semantic-anchored fusion (Sec. 3.2.1, Eq. 4 group means plus the
 // additive anchor, Eq. 5 order) as a segmented mean over K/V rows.
+// Head sizes 64 and 128 (K/V-space fusion) use the lane-group kernel below;
+// wider rows -- the embedding-space form, one "head" of width d_model -- use
+// a kernel with one block per span that sweeps the row in 16-byte columns.
+// Either kernel fuses K and V, or K alone when no V is given.
 //
 // Work split: a "lane group" of D/ (16 bytes / element size) lanes owns one
 // (layer, KV head, K-or-V, span); each lane owns 16 contiguous bytes of the
@@ -23,6 +27,8 @@ struct FuseArgs {
     float* score_out;
     int32_t* pos_out;
     int32_t H;
+    int32_t kinds;              // 2: K and V, 1: K only
+    int32_t d;                  // row length (the wide-row kernel)
     int32_t T_in, n_spans;      // single sequence
     int64_t in_plane, out_plane;  // rows per (layer, head) plane of the input and of the output
     int32_t blocks_per_seq;     // ragged: span blocks per sequence in grid x
@@ -63,8 +69,8 @@ __global__ __launch_bounds__(256) void fuse_spans_kernel(const FuseArgs a) {
 
     const int sub = threadIdx.x / LANES;
     const int lane = threadIdx.x % LANES;
-    const int which = blockIdx.y & 1;    // 0: K, 1: V
-    const int h = blockIdx.y >> 1;
+    const int which = blockIdx.y % a.kinds;  // 0: K, 1: V
+    const int h = blockIdx.y / a.kinds;
     const int l = blockIdx.z;
     int bx = blockIdx.x, T_in = a.T_in, n_spans = a.n_spans;
     int64_t in_row = 0, out_row = 0;  // first row of the sequence in its planes
@@ -140,6 +146,106 @@ __global__ __launch_bounds__(256) void fuse_spans_kernel(const FuseArgs a) {
     }
 }
 
+// Wide rows (d a multiple of one 16-byte vector, other than 64 and 128): one
+// block of WIDE_THREADS threads per (span, K-or-V, head, layer); thread t
+// owns the 16-byte columns t, t + WIDE_THREADS, ... of the row and sums them
+// over the span's rows in row order (4 rows in flight), as the lane-group
+// kernel does, so the arithmetic is the same.
+constexpr int WIDE_THREADS = 256;
+template <int DT, bool RAG>
+__global__ __launch_bounds__(WIDE_THREADS) void fuse_wide_kernel(const FuseArgs a) {
+    using E = vz::Elem<DT>;
+    using T = typename E::T;
+    constexpr int PER = E::kPer16B;
+    const int nv = a.d / PER;  // 16-byte columns per row
+    const int which = blockIdx.y % a.kinds;
+    const int h = blockIdx.y / a.kinds;
+    const int l = blockIdx.z;
+    int64_t j = blockIdx.x;
+    int T_in = a.T_in, n_spans = a.n_spans;
+    int64_t in_row = 0, out_row = 0;
+    const int32_t* off = a.off;
+    if constexpr (RAG) {
+        const int s = static_cast<int>(blockIdx.x / a.blocks_per_seq);
+        j = blockIdx.x - static_cast<int64_t>(s) * a.blocks_per_seq;
+        const int st = ragged_fuse_status(a, s);
+        if (a.status && j == 0 && blockIdx.y == 0 && l == 0 && threadIdx.x == 0) a.status[s] = st;
+        if (st != VZ_OK) return;
+        T_in = a.T_in_s[s];
+        n_spans = a.n_spans_s[s];
+        in_row = a.in_base[s];
+        out_row = a.base[s];
+        off = a.off + a.off_base[s];
+    }
+    if (j >= n_spans) return;
+    int32_t b = off[j], e = off[j + 1];
+    b = b < 0 ? 0 : (b > T_in ? T_in : b);
+    e = e < b ? b : (e > T_in ? T_in : e);
+    const float cnt = static_cast<float>(e - b);
+    const T* src = static_cast<const T*>(which ? a.v_in : a.k_in) +
+                   ((static_cast<size_t>(l) * a.H + h) * static_cast<size_t>(a.in_plane) + in_row) * a.d;
+    const T* anchor = static_cast<const T*>(which ? a.av : a.ak);
+    const size_t orow = (static_cast<size_t>(l) * a.H + h) * static_cast<size_t>(a.out_plane) + out_row + j;
+    const size_t arow = RAG ? orow : (static_cast<size_t>(l) * a.H + h) * static_cast<size_t>(n_spans) + j;
+    T* dst = static_cast<T*>(which ? a.v_out : a.k_out) + orow * a.d;
+    for (int c = threadIdx.x; c < nv; c += WIDE_THREADS) {
+        const T* col = src + c * PER;
+        float acc[PER];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) acc[i] = 0.f;
+        int32_t r = b;
+        for (; r + 4 <= e; r += 4) {
+            uint4 x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const uint4*>(col + static_cast<size_t>(r + u) * a.d);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                float f[PER];
+                vz::unpack16<DT>(x[u], f);
+#pragma unroll
+                for (int i = 0; i < PER; ++i) acc[i] += f[i];
+            }
+        }
+        for (; r < e; ++r) {
+            const uint4 x = *reinterpret_cast<const uint4*>(col + static_cast<size_t>(r) * a.d);
+            float f[PER];
+            vz::unpack16<DT>(x, f);
+#pragma unroll
+            for (int i = 0; i < PER; ++i) acc[i] += f[i];
+        }
+#pragma unroll
+        for (int i = 0; i < PER; ++i) acc[i] = (e > b) ? acc[i] / cnt : 0.f;
+        if (anchor) {
+            const uint4 x = *reinterpret_cast<const uint4*>(anchor + arow * a.d + c * PER);
+            float f[PER];
+            vz::unpack16<DT>(x, f);
+#pragma unroll
+            for (int i = 0; i < PER; ++i) acc[i] += f[i];
+        }
+        *reinterpret_cast<uint4*>(dst + c * PER) = vz::pack16<DT>(acc);
+    }
+    if (which == 0 && h == 0 && threadIdx.x == 0) {
+        const size_t prow = static_cast<size_t>(l) * a.out_plane + out_row + j;
+        a.pos_out[prow] = static_cast<int32_t>(j);
+        a.score_out[prow] = 0.f;
+    }
+}
+
+template <int DT>
+hipError_t launch_wide(const FuseArgs& a, int32_t L, hipStream_t stream) {
+    if (a.n_seqs > 0) {
+        FuseArgs r = a;
+        r.blocks_per_seq = a.max_spans > 0 ? a.max_spans : 1;  // still report every sequence's status
+        dim3 grid(static_cast<unsigned>(static_cast<int64_t>(r.blocks_per_seq) * a.n_seqs), a.kinds * a.H, L);
+        hipLaunchKernelGGL((fuse_wide_kernel<DT, true>), grid, dim3(WIDE_THREADS), 0, stream, r);
+        return hipGetLastError();
+    }
+    if (a.n_spans == 0) return hipSuccess;
+    dim3 grid(a.n_spans, a.kinds * a.H, L);
+    hipLaunchKernelGGL((fuse_wide_kernel<DT, false>), grid, dim3(WIDE_THREADS), 0, stream, a);
+    return hipGetLastError();
+}
+
 template <int DT, int D>
 hipError_t launch(const FuseArgs& a, int32_t L, hipStream_t stream) {
     constexpr int SPB = 256 / (D / vz::Elem<DT>::kPer16B);
@@ -147,21 +253,25 @@ hipError_t launch(const FuseArgs& a, int32_t L, hipStream_t stream) {
         FuseArgs r = a;
         r.blocks_per_seq = (a.max_spans + SPB - 1) / SPB;
         if (r.blocks_per_seq == 0) r.blocks_per_seq = 1;  // still report every sequence's status
-        dim3 grid(static_cast<unsigned>(static_cast<int64_t>(r.blocks_per_seq) * a.n_seqs), 2 * a.H, L);
+        dim3 grid(static_cast<unsigned>(static_cast<int64_t>(r.blocks_per_seq) * a.n_seqs), a.kinds * a.H, L);
         hipLaunchKernelGGL((fuse_spans_kernel<DT, D, true>), grid, dim3(256), 0, stream, r);
         return hipGetLastError();
     }
     if (a.n_spans == 0) return hipSuccess;
-    dim3 grid((a.n_spans + SPB - 1) / SPB, 2 * a.H, L);
+    dim3 grid((a.n_spans + SPB - 1) / SPB, a.kinds * a.H, L);
     hipLaunchKernelGGL((fuse_spans_kernel<DT, D, false>), grid, dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
-hipError_t dispatch(const FuseArgs& a, int32_t L, int32_t d, int32_t dtype, hipStream_t stream) {
+hipError_t dispatch(FuseArgs a, int32_t L, int32_t d, int32_t dtype, hipStream_t stream) {
+    a.kinds = a.v_in ? 2 : 1;
+    a.d = d;
     if (dtype == VZ_BF16 && d == 128) return launch<VZ_BF16, 128>(a, L, stream);
     if (dtype == VZ_BF16 && d == 64) return launch<VZ_BF16, 64>(a, L, stream);
     if (dtype == VZ_F32 && d == 128) return launch<VZ_F32, 128>(a, L, stream);
     if (dtype == VZ_F32 && d == 64) return launch<VZ_F32, 64>(a, L, stream);
+    if (dtype == VZ_BF16 && d % vz::Elem<VZ_BF16>::kPer16B == 0) return launch_wide<VZ_BF16>(a, L, stream);
+    if (dtype == VZ_F32 && d % vz::Elem<VZ_F32>::kPer16B == 0) return launch_wide<VZ_F32>(a, L, stream);
     return hipErrorInvalidValue;
 }
 

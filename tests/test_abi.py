@@ -61,6 +61,7 @@ def _decode(**kw):
     (dict(L=0), vz.VZ_ERR_SHAPE),
     (dict(Hq=68, Hkv=4), vz.VZ_ERR_UNSUPPORTED),
     (dict(d=96), vz.VZ_ERR_UNSUPPORTED),
+    (dict(d=256), vz.VZ_ERR_UNSUPPORTED),    # wide rows are for fusion only
     (dict(dtype=7), vz.VZ_ERR_UNSUPPORTED),
     (dict(ws=None), vz.VZ_ERR_WORKSPACE),
     (dict(ws_bytes=16), vz.VZ_ERR_WORKSPACE),
@@ -120,7 +121,12 @@ def _fuse(**kw):
     (dict(vo=ctypes.c_void_p(0x400000 + 256)), vz.VZ_ERR_INVALID),  # v_out overlaps k_out
     (dict(n=33), vz.VZ_ERR_CAPACITY),
     (dict(n=101, cap=200), vz.VZ_ERR_SHAPE),
-    (dict(d=100), vz.VZ_ERR_UNSUPPORTED),
+    (dict(d=102), vz.VZ_ERR_UNSUPPORTED),                          # float32 rows: a multiple of 4 elements
+    (dict(d=100, dtype=vz.VZ_BF16), vz.VZ_ERR_UNSUPPORTED),        # bf16 rows: a multiple of 8 elements
+    (dict(d=16392, dtype=vz.VZ_BF16), vz.VZ_ERR_UNSUPPORTED),      # wider than 16384
+    (dict(vi=None), vz.VZ_ERR_INVALID),                            # v_out without v_in
+    (dict(vo=None), vz.VZ_ERR_INVALID),                            # v_in without v_out
+    (dict(vi=None, vo=None, ak=FAKE, av=FAKE), vz.VZ_ERR_INVALID),  # anchor_v without v_in
 ])
 def test_fuse_rejects(kw, code):
     assert _fuse(**kw) == code
@@ -217,7 +223,9 @@ def _fuse_ragged(**kw):
     (dict(max_spans=65), vz.VZ_ERR_SHAPE),                          # more spans than output slots
     (dict(total_off=0), vz.VZ_ERR_SHAPE),
     (dict(n=0), vz.VZ_ERR_SHAPE),
-    (dict(d=100), vz.VZ_ERR_UNSUPPORTED),
+    (dict(d=102), vz.VZ_ERR_UNSUPPORTED),
+    (dict(vi=None), vz.VZ_ERR_INVALID),
+    (dict(vi=None, vo=None, ak=FAKE, av=FAKE), vz.VZ_ERR_INVALID),
 ])
 def test_fuse_ragged_rejects(kw, code):
     assert _fuse_ragged(**kw) == code

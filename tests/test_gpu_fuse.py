@@ -113,3 +113,121 @@ def test_fuse_with_offsets_from_the_span_builder():
     y = synth.as_storage(synth.normal_f32(synth.stream_key(key, "v"), L * H * L_a * d).reshape(L, H, L_a, d), dtype)
     _, k, v, s, p, sen = _run(x, y, off, dtype, len(off) + 7)
     _verify(x, y, off, dtype, k, v, s, p, sen)
+
+
+def _fuse_wide(x_k, x_v, off, dtype, cap, anchor_k=None, anchor_v=None):
+    """Direct call for row sizes the decode path does not take (no workspaces)."""
+    import torch
+    import paper_2608_08569_amd as vz
+    L, H, T, d = x_k.shape
+    tdt = torch.float32 if dtype == synth.DT_F32 else torch.bfloat16
+    sentinel = 7.0
+    k_out = torch.full((L, H, cap, d), sentinel, dtype=tdt, device="cuda")
+    v_out = None if x_v is None else torch.full((L, H, cap, d), sentinel, dtype=tdt, device="cuda")
+    score = torch.full((L, cap), -1.0, dtype=torch.float32, device="cuda")
+    pos = torch.full((L, cap), -5, dtype=torch.int32, device="cuda")
+    dev = lambda a: None if a is None else to_dev(a)
+    vz.voxzip_fuse_spans(to_dev(x_k), dev(x_v), to_dev(off), k_out, v_out, score, pos,
+                         anchor_k=dev(anchor_k), anchor_v=dev(anchor_v))
+    torch.cuda.synchronize()
+    return from_dev(k_out), None if v_out is None else from_dev(v_out), from_dev(score), from_dev(pos), sentinel
+
+
+@pytest.mark.parametrize("dtype,d", [(synth.DT_BF16, 256), (synth.DT_BF16, 1000), (synth.DT_BF16, 3584),
+                                     (synth.DT_F32, 260), (synth.DT_F32, 2048)])
+@pytest.mark.parametrize("with_anchor", [False, True])
+def test_fuse_wide_rows(dtype, d, with_anchor):
+    """Row sizes other than 64 and 128 (the wide-row kernel): K and V, span
+    lengths 1..13 (tails of the 4-row unroll), columns past one block of
+    threads (3584 bf16 = 448 vectors), against the oracle."""
+    L, H = 2, 2
+    key = synth.stream_key(17, "fuse-wide", dtype, d)
+    lens = synth.uniform_int(key, 0, 45, 1, 14)
+    lens[::5] = 1
+    off = synth.offsets_from_lengths(lens)
+    T, n = int(off[-1]), len(lens)
+    mk = lambda tag, shape: synth.as_storage(
+        synth.normal_f32(synth.stream_key(key, tag), int(np.prod(shape))).reshape(shape) * np.float32(1.5), dtype)
+    k_in, v_in = mk("k", (L, H, T, d)), mk("v", (L, H, T, d))
+    anchor = (mk("ak", (L, H, n, d)), mk("av", (L, H, n, d))) if with_anchor else None
+    k, v, s, p, sen = _fuse_wide(k_in, v_in, off, dtype, n + 5, *(anchor or (None, None)))
+    _verify(k_in, v_in, off, dtype, k, v, s, p, sen, anchor=anchor)
+
+
+def test_embedding_space_stage1():
+    """Sec. 3.2.1 in its literal, embedding-space form: ASR segments (with
+    low-confidence and overlapping ones) give the span offsets through the
+    library's span builder, the audio-token embeddings [L_a][d_model] are
+    pooled per span and the text-token embeddings are added as anchors (zero
+    rows for background tokens, which the kernel then copies bit for bit);
+    one tensor only (v_in = v_out = NULL), d_model = 3584, bf16."""
+    import paper_2608_08569_amd as vz
+    dtype, d_model, L_a, t_total = synth.DT_BF16, 3584, 1500, 30000
+    key = synth.stream_key(23, "embedding-stage1")
+    n_seg = 14
+    u = synth.uniform01(key, 0, 4 * n_seg)
+    ts = np.sort((u[:n_seg] * t_total * 0.95).astype(np.int64))
+    te = ts + (400 + u[n_seg:2 * n_seg] * 2600).astype(np.int64)
+    conf = (0.1 + 0.9 * u[2 * n_seg:3 * n_seg]).astype(np.float32)
+    tl = (1 + u[3 * n_seg:4 * n_seg] * 25).astype(np.int32)
+    off = vz.voxzip_build_span_offsets(ts, te, conf, tl, t_total, L_a, 0.3)
+    assert np.array_equal(off, oracle.build_offsets(ts, te, conf, tl, t_total, L_a, 0.3))
+    n = len(off) - 1
+    lens = np.diff(off)
+    assert 1 < n < L_a and lens.max() > 1
+    emb = synth.as_storage(synth.normal_f32(synth.stream_key(key, "audio"), L_a * d_model).reshape(
+        1, 1, L_a, d_model), dtype)
+    text = synth.as_storage(synth.normal_f32(synth.stream_key(key, "text"), n * d_model).reshape(
+        1, 1, n, d_model) * np.float32(0.5), dtype)
+    text[:, :, lens == 1] = 0           # background (and one-token) spans carry no text anchor
+    k, v, s, p, sen = _fuse_wide(emb, None, off, dtype, n + 3, anchor_k=text)
+    assert v is None
+    ref = oracle.fuse(emb, off, dtype, anchor=text)
+    got = widen(k[:, :, :n], dtype)
+    check_close(got, ref, RTOL[dtype], "fused embeddings")
+    assert np.all(np.abs(got - ref) <= bf16_ulp(ref) + 1e-6 * np.abs(ref))
+    one = np.nonzero(lens == 1)[0]
+    assert np.array_equal(k[:, :, one], emb[:, :, off[one]])        # copies, bit for bit
+    assert np.all(widen(k[:, :, n:], dtype) == sen)
+    assert np.array_equal(p[0, :n], np.arange(n, dtype=np.int32)) and np.all(s[0, :n] == 0)
+
+
+def test_fuse_ragged_wide_rows_k_only():
+    """The ragged twin with wide rows and k alone: three sequences of
+    embeddings (d_model = 1024, bf16) fused into one packed output."""
+    import torch
+    import paper_2608_08569_amd as vz
+    dtype, d, L, H = synth.DT_BF16, 1024, 1, 1
+    key = synth.stream_key(29, "fuse-ragged-wide")
+    T_in = [37, 1, 90]
+    lens = [synth.uniform_int(synth.stream_key(key, "lens", i), 0, t, 1, 6) for i, t in enumerate(T_in)]
+    offs = []
+    for t, ln in zip(T_in, lens):
+        o = synth.offsets_from_lengths(ln)
+        o = o[o <= t]
+        if o[-1] != t:
+            o = np.append(o, t)
+        offs.append(o.astype(np.int32))
+    n_sp = [len(o) - 1 for o in offs]
+    in_base = np.concatenate([[0], np.cumsum(T_in)[:-1]]).astype(np.int64)
+    off_base = np.concatenate([[0], np.cumsum([len(o) for o in offs])[:-1]]).astype(np.int64)
+    caps = [n + 2 for n in n_sp]
+    seq_base = np.concatenate([[0], np.cumsum(caps)[:-1]]).astype(np.int64)
+    total_in, total = int(sum(T_in)), int(sum(caps))
+    x = synth.as_storage(synth.normal_f32(synth.stream_key(key, "x"), total_in * d).reshape(L, H, total_in, d), dtype)
+    anc = synth.as_storage(synth.normal_f32(synth.stream_key(key, "a"), total * d).reshape(L, H, total, d), dtype)
+    dev = lambda a, dt: torch.tensor(np.asarray(a), dtype=dt, device="cuda")
+    k_out = torch.zeros(L, H, total, d, dtype=torch.bfloat16, device="cuda")
+    score = torch.zeros(L, total, dtype=torch.float32, device="cuda")
+    pos = torch.zeros(L, total, dtype=torch.int32, device="cuda")
+    status = torch.full((3,), 99, dtype=torch.int32, device="cuda")
+    vz.voxzip_fuse_spans_ragged(to_dev(x), None, dev(in_base, torch.int64), dev(T_in, torch.int32),
+                                to_dev(np.concatenate(offs)), dev(off_base, torch.int64), dev(n_sp, torch.int32),
+                                max(n_sp), k_out, None, score, pos, dev(seq_base, torch.int64),
+                                dev(caps, torch.int32), status=status, anchor_k=to_dev(anc))
+    assert np.all(from_dev(status) == 0)
+    k = from_dev(k_out)
+    for i in range(3):
+        n, b, ib = n_sp[i], int(seq_base[i]), int(in_base[i])
+        ref = oracle.fuse(x[:, :, ib:ib + T_in[i]], offs[i], dtype, anchor=anc[:, :, b:b + n])
+        check_close(widen(k[:, :, b:b + n], dtype), ref, RTOL[dtype], f"sequence {i}")
