@@ -41,13 +41,21 @@ constexpr int RO_STRIDE = D + 4;                   // padded LDS row of a wave's
 // chunks, so the last chunk of a row is written whole).
 inline __host__ __device__ int64_t range_row(int64_t plane) { return (plane + CHUNK - 1) / CHUNK * CHUNK; }
 
+// Row of key r (0..CHUNK-1) in a chunk's [key][head] half-precision rows
+// (16 bytes each): bit 1 is flipped by bit 4, so that the 8 keys one write
+// instruction covers (r = c + 4 q4 + 16 hi) start on 8 distinct 4-bank groups.
+__device__ __forceinline__ int pslot(int r) { return r ^ ((r >> 3) & 2); }
+
 template <int NW>
 __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArgs a) {
     static_assert(RW * GMAX * RO_STRIDE * 4 <= RW * TILE_BYTES, "the merged outputs fit in the tile buffers");
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[RW][TILE_BYTES];
     __shared__ float2 s_stat[RW][GMAX];
-    __shared__ uint4 s_pst[RW][RLDS][2][64];  // p~ of the first RLDS chunks: [wave][chunk][half][lane]
-    __shared__ float s_mref[RW][RNCH][GMAX];  // reference max of each chunk's p~, per head
+    // p~ of the first RLDS chunks of each wave, transposed: [slot(key)][head]
+    // in half precision (16 bytes per key; slot() in the head-sum epilogue)
+    __shared__ __attribute__((aligned(16))) uint16_t s_pt[RW][RLDS][CHUNK][GMAX];
+    __shared__ __attribute__((aligned(16))) float s_mref[RW][RNCH][GMAX];  // reference max of each chunk's p~, per head (then its factor)
+    __shared__ float2 s_MS[GMAX];             // the workgroup's max M and 1 / sum S, per head
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int q4 = lane >> 4, r16 = lane & 15;
@@ -234,8 +242,15 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
             pk[2 * u + 1] = pack_f16x2(sp[u][2], sp[u][3]);
         }
         if (k < RLDS) {
-            s_pst[w][k][0][lane] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
-            s_pst[w][k][1][lane] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+            // written as [key][head] rows now, while the wave waits for memory
+            // anyway, so that the epilogue only reads whole rows
+            uint16_t* const pt = &s_pt[w][k][0][0];
+#pragma unroll
+            for (int u = 0; u < PAIRS; ++u)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    pt[pslot(VT * u + 16 * hi + 4 * q4 + i) * GMAX + hh] =
+                        static_cast<uint16_t>(pk[2 * u + (i >> 1)] >> (16 * (i & 1)));
         } else if (k < RFULL) {
 #pragma unroll
             for (int i = 0; i < 2 * PAIRS; ++i) pst[k - RLDS][i] = pk[i];
@@ -259,6 +274,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         S = fmaf(st.y, st.x == -INFINITY ? 0.f : exp2f(st.x - M), S);
     }
     const float inv_S = 1.0f / S;
+    if (w == 0 && q4 == 0 && hi == 0) s_MS[hh] = make_float2(M, inv_S);  // read after the next barrier
 
     // ---- output rows: the waves' outputs, rescaled, summed in wave order ----
     float* const s_o = reinterpret_cast<float*>(&s_tile[0][0]);  // [RW][GMAX][RO_STRIDE]
@@ -280,52 +296,60 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     }
 
     // ---- each key's sum over this KV head's query heads of p_hj ----
-    // Per chunk, each lane scales its values (one head, 16 keys) and writes
-    // them to the wave's LDS scratch as [key][head] rows; each lane then reads
-    // two keys' rows back and adds them.  The key slots are XOR-swizzled so
-    // that the 8 keys of one write instruction fall on 8 distinct bank groups.
-    // (LDS operations of a wave complete in order, so the wave needs no
-    // barrier between its own writes and reads.)
-    __syncthreads();  // the output merge has read the tile buffers
-    static_assert(CHUNK * GMAX * 4 <= TILE_BYTES, "a chunk's rows fit in the wave's tile buffer");
-    float* const xs = reinterpret_cast<float*>(s_tile[w]);  // [CHUNK][GMAX] floats of this wave
-    auto slot = [](int r) { return r ^ ((r >> 3) & 3); };
+    // Every chunk's p~ ends up as [slot(key)][head] half-precision rows: the
+    // LDS-resident chunks were written so in the loop, the register-held ones
+    // are written to the wave's (now free) tile buffer here.  Each lane then
+    // reads two keys' rows and forms sum_h p~_h * f_h with f_h =
+    // exp2(m_ref,h - M_h) / S_h from a per-chunk factor table.  (LDS
+    // operations of a wave complete in order: no barrier between a wave's own
+    // writes and reads.)
+    __syncthreads();  // the output merge has read the tile buffers; s_MS is written
     float* const gsum = reinterpret_cast<float*>(a.ws + a.hdr_bytes) + (static_cast<size_t>(l) * NW + g) * range_row(a.plane);
-    const float fh = hh < G ? inv_S : 0.f;
+    // factor table, in place of the reference maxima: f[k][h]
+    for (int e = lane; e < RNCH * GMAX; e += 64) {
+        const int k = e / GMAX, h = e - k * GMAX;
+        if (k < my_chunks) {
+            const float2 ms = s_MS[h];
+            s_mref[w][k][h] = h < G ? exp2f(s_mref[w][k][h] - ms.x) * ms.y : 0.f;
+        }
+    }
+    uint16_t* const scratch = reinterpret_cast<uint16_t*>(s_tile[w]);  // [CHUNK][GMAX] halves
 #pragma unroll 1
     for (int k = 0; k < my_chunks; ++k) {
-        const float f = exp2f(s_mref[w][k][hh] - M) * fh;
-        uint32_t pk[2 * PAIRS];
-        if (k < RLDS) {
-            const uint4 p0 = s_pst[w][k][0][lane], p1 = s_pst[w][k][1][lane];
-            pk[0] = p0.x, pk[1] = p0.y, pk[2] = p0.z, pk[3] = p0.w;
-            pk[4] = p1.x, pk[5] = p1.y, pk[6] = p1.z, pk[7] = p1.w;
-        } else {
+        const uint16_t* rows = &s_pt[w][k < RLDS ? k : 0][0][0];
+        if (k >= RLDS) {
+            uint32_t pk[2 * PAIRS];
             pk[0] = pst_last[0];
             pk[1] = pst_last[1];
 #pragma unroll
             for (int i = 2; i < 2 * PAIRS; ++i) pk[i] = 0;  // keys past the cache: p~ = 0
+#pragma unroll
+            for (int r = 0; r < RFULL - RLDS; ++r)  // register slots: fixed indexes, wave-uniform choice
+                if (k == RLDS + r) {
+#pragma unroll
+                    for (int i = 0; i < 2 * PAIRS; ++i) pk[i] = pst[r][i];
+                }
+#pragma unroll
+            for (int u = 0; u < PAIRS; ++u)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    scratch[pslot(VT * u + 16 * hi + 4 * q4 + i) * GMAX + hh] =
+                        static_cast<uint16_t>(pk[2 * u + (i >> 1)] >> (16 * (i & 1)));
+            rows = scratch;
         }
-#pragma unroll
-        for (int r = 0; r < RFULL - RLDS; ++r)  // register slots: fixed indexes, wave-uniform choice
-            if (k == RLDS + r) {
-#pragma unroll
-                for (int i = 0; i < 2 * PAIRS; ++i) pk[i] = pst[r][i];
-            }
-#pragma unroll
-        for (int u = 0; u < PAIRS; ++u)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint16_t h16 = static_cast<uint16_t>(pk[2 * u + (i >> 1)] >> (16 * (i & 1)));
-                const int key = VT * u + 16 * hi + 4 * q4 + i;
-                xs[slot(key) * GMAX + hh] = f16_to_f32(h16) * f;
-            }
+        const float4 fa = *reinterpret_cast<const float4*>(&s_mref[w][k][0]);
+        const float4 fb = *reinterpret_cast<const float4*>(&s_mref[w][k][4]);
+        const float fk[GMAX] = {fa.x, fa.y, fa.z, fa.w, fb.x, fb.y, fb.z, fb.w};
         float y[2];
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-            const float4* row = reinterpret_cast<const float4*>(xs + slot(2 * lane + e) * GMAX);
-            const float4 a0 = row[0], a1 = row[1];
-            y[e] = ((a0.x + a0.y) + (a0.z + a0.w)) + ((a1.x + a1.y) + (a1.z + a1.w));
+            const uint4 r = *reinterpret_cast<const uint4*>(rows + pslot(2 * lane + e) * GMAX);
+            const uint32_t wd[4] = {r.x, r.y, r.z, r.w};
+            float acc = 0.f;
+#pragma unroll
+            for (int h = 0; h < GMAX; ++h)
+                acc = fmaf(f16_to_f32(static_cast<uint16_t>(wd[h >> 1] >> (16 * (h & 1)))), fk[h], acc);
+            y[e] = acc;
         }
         *reinterpret_cast<float2*>(gsum + chunk_of(k) * CHUNK + 2 * lane) = make_float2(y[0], y[1]);
     }
