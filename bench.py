@@ -142,7 +142,7 @@ class Sequence:
         self.P = torch.zeros(L, self.cap, dtype=torch.int32, device="cuda")
         self.out = torch.zeros(L, Hq, d, dtype=bf, device="cuda")
         self.ws_d = vz.workspace(vz.VZ_OP_DECODE, L, Hq, Hkv, d, self.cap)
-        self.ws_e = vz.workspace(vz.VZ_OP_EVICT, L, Hq, Hkv, d, self.cap)
+        self.ws_s = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, self.cap)
 
     def start(self):
         self.vz.voxzip_fuse_spans(self.k_in, self.v_in, self.off, self.K, self.V, self.S, self.P,
@@ -155,16 +155,17 @@ class Sequence:
         w, vz = self.w, self.vz
         L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
         q, kn, vn = self.steps_in[t]
-        vz.voxzip_decode_attend_score(q, kn, vn, self.K, self.V, self.S, self.P, self.out, self.len, self.nxt,
-                                      w.gamma, workspace=self.ws_d, stream=self.stream)
         T = self.len + 1
         b = L * decode_bytes_per_layer(T, Hq, Hkv, d, 2)
-        self.len, self.nxt = T, self.nxt + 1
-        if (t + 1) % w.interval == 0 and self.len > w.budget:
-            E = self.len - w.budget
-            self.len = vz.voxzip_evict_compact(self.K, self.V, self.S, self.P, self.len, w.budget, self.nxt,
-                                               workspace=self.ws_e, stream=self.stream)
-            b += L * evict_bytes_per_layer(T, E, Hkv, d, 2)
+        if (t + 1) % w.interval == 0 and T > w.budget:  # a step with its eviction: one call
+            new_len = vz.voxzip_decode_evict(q, kn, vn, self.K, self.V, self.S, self.P, self.out, self.len,
+                                             self.nxt, w.gamma, w.budget, workspace=self.ws_s, stream=self.stream)
+            b += L * evict_bytes_per_layer(T, T - w.budget, Hkv, d, 2)
+        else:
+            vz.voxzip_decode_attend_score(q, kn, vn, self.K, self.V, self.S, self.P, self.out, self.len, self.nxt,
+                                          w.gamma, workspace=self.ws_d, stream=self.stream)
+            new_len = T
+        self.len, self.nxt = new_len, self.nxt + 1
         return b
 
 
@@ -420,6 +421,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5, help="timed requests")
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--decode-steps", type=int, default=256)
+    ap.add_argument("--roofline-calls", type=int, default=64,
+                    help="decode calls at the steady length timed for the roofline")
     ap.add_argument("--cpu-layers", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
@@ -483,11 +486,12 @@ def main():
     S = torch.zeros(L, cap, dtype=torch.float32, device="cuda")
     P = torch.zeros(L, cap, dtype=torch.int32, device="cuda")
     out = torch.zeros(L, Hq, d, dtype=torch.bfloat16, device="cuda")
+    ws_step = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
     ws_d = vz.workspace(vz.VZ_OP_DECODE, L, Hq, Hkv, d, cap)
-    ws_e = vz.workspace(vz.VZ_OP_EVICT, L, Hq, Hkv, d, cap)
 
     def request(timing=None):
-        """Fuse, then decode with eviction; returns (decode tokens, bytes)."""
+        """Fuse, then one generation step per token (decode + eviction in one
+        call); returns (decode tokens, bytes)."""
         ev = timing
         if ev is not None:
             ev["fuse"][0].record(stream)
@@ -498,19 +502,14 @@ def main():
         total_bytes = 0
         for t in range(args.decode_steps):
             q, kn, vn = steps_in[t]
-            if ev is not None:
-                ev["dec"][t][0].record(stream)
-            vz.voxzip_decode_attend_score(q, kn, vn, K, V, S, P, out, length, nxt, w.gamma, workspace=ws_d)
-            if ev is not None:
-                ev["dec"][t][1].record(stream)
+            new_len = vz.voxzip_decode_evict(q, kn, vn, K, V, S, P, out, length, nxt, w.gamma, w.budget,
+                                             workspace=ws_step)
             T = length + 1
             total_bytes += L * decode_bytes_per_layer(T, Hq, Hkv, d, s)
-            length, nxt = T, nxt + 1
-            if length > w.budget:
-                E = length - w.budget
-                length = vz.voxzip_evict_compact(K, V, S, P, length, w.budget, nxt, workspace=ws_e)
-                total_bytes += L * evict_bytes_per_layer(T, E, Hkv, d, s)
-        return args.decode_steps, total_bytes
+            if T > w.budget:
+                total_bytes += L * evict_bytes_per_layer(T, T - w.budget, Hkv, d, s)
+            length, nxt = new_len, nxt + 1
+        return args.decode_steps, total_bytes, length, nxt
 
     for _ in range(args.warmup):
         request()
@@ -523,22 +522,46 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
-        ev = {"fuse": (mk(), mk()), "dec": [(mk(), mk()) for _ in range(args.decode_steps)]}
-        tk, b = request(ev)
+        ev = {"fuse": (mk(), mk())}  # no per-step events in the timed requests: each costs a pipeline drain
+        tk, b, length, nxt = request(ev)
         tokens += tk
         path_bytes += b
         timings.append(ev)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
 
-    dec_ms = np.array([[a.elapsed_time(b) for a, b in ev["dec"]] for ev in timings])  # [req][step]
     fuse_ms = np.array([ev["fuse"][0].elapsed_time(ev["fuse"][1]) for ev in timings])
-    # dominant kernel: decode over all layers at the steady-state length T = B + 1
+    # Dominant kernel: the decode entry point over all layers at the steady
+    # length T = B + 1, timed with HIP events on its own after the requests
+    # (the requests run it fused with the eviction), from the final state.
     T_ss = w.budget + 1
+    assert length == w.budget
     dec_bytes_ss = L * decode_bytes_per_layer(T_ss, Hq, Hkv, d, s)
-    steady = dec_ms[:, 16:] if dec_ms.shape[1] > 32 else dec_ms
-    dec_mean_s = float(np.mean(steady)) * 1e-3
+    q, kn, vn = steps_in[-1]
+    for _ in range(4):
+        vz.voxzip_decode_attend_score(q, kn, vn, K, V, S, P, out, length, nxt, w.gamma, workspace=ws_d)
+    dec_ev = [(mk(), mk()) for _ in range(args.roofline_calls)]
+    for a, b in dec_ev:
+        a.record(stream)
+        vz.voxzip_decode_attend_score(q, kn, vn, K, V, S, P, out, length, nxt, w.gamma, workspace=ws_d)
+        b.record(stream)
+    torch.cuda.synchronize()
+    dec_ms = np.array([a.elapsed_time(b) for a, b in dec_ev])
+    dec_mean_s = float(np.mean(dec_ms)) * 1e-3
     achieved = dec_bytes_ss / dec_mean_s / 1e9
+    # the generation step (decode + one eviction per layer) at the same length,
+    # continuing the request's sequence
+    step_ev = [(mk(), mk()) for _ in range(args.roofline_calls)]
+    for i, (a, b) in enumerate(step_ev):
+        q, kn, vn = steps_in[i % len(steps_in)]
+        a.record(stream)
+        length = vz.voxzip_decode_evict(q, kn, vn, K, V, S, P, out, length, nxt, w.gamma, w.budget,
+                                        workspace=ws_step)
+        b.record(stream)
+        nxt += 1
+    torch.cuda.synchronize()
+    step_ms = np.array([a.elapsed_time(b) for a, b in step_ev])
+    step_bytes_ss = dec_bytes_ss + L * evict_bytes_per_layer(T_ss, 1, Hkv, d, s)
     traffic = read_traffic()
     fuse_bytes = L * Hkv * 2 * (32768 + n_spans) * d * s
 
@@ -559,13 +582,16 @@ def main():
             "workload": "long32k",
             "description": (f"48 layers, 32Q/4KV heads, d=128, bf16 KV cache; 32768 audio tokens fused to "
                             f"{n_spans} span tokens (Stage 1), B=8192 (M=1638, N=6550, T=4), gamma=0.95; "
-                            f"one step = fusion + {args.decode_steps} decode steps with eviction"),
+                            f"one step = fusion + {args.decode_steps} generation steps (decode + eviction, "
+                            f"one voxzip_decode_evict call each)"),
             "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "audio_tokens": 32768,
             "fused_tokens": n_spans, "budget": w.budget, "decode_steps_per_request": args.decode_steps,
         },
         "path_gbps": path_bytes / elapsed / 1e9,
         "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
-        "decode_us_mean": float(np.mean(dec_ms)) * 1e3,
+        "step_us_steady": float(np.mean(step_ms)) * 1e3,
+        "step_gbps_steady": step_bytes_ss / (float(np.mean(step_ms)) * 1e-3) / 1e9,
+        "decode_us_mean": dec_mean_s * 1e6,
         "fuse_ms_mean": float(np.mean(fuse_ms)),
         "fuse_gbps": fuse_bytes / (float(np.mean(fuse_ms)) * 1e-3) / 1e9,
         "roofline": {
@@ -579,6 +605,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": dec_bytes_ss,
             "mean_launch_us": dec_mean_s * 1e6,
+            "launches_timed": args.roofline_calls,
         },
     }
     if not args.no_cpu:

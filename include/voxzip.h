@@ -53,6 +53,7 @@ extern "C" {
 /* Operations whose workspace can be queried. */
 #define VZ_OP_DECODE 1
 #define VZ_OP_EVICT 2
+#define VZ_OP_DECODE_EVICT 3   /* voxzip_decode_evict */
 
 /*
  * Stage-1 span offsets (Sec. 3.2.1: confidence filter, Eq. 3 time-to-token
@@ -186,6 +187,35 @@ VZ_API int voxzip_evict_compact(void *k_cache, void *v_cache, float *score, int3
                          int32_t next_pos, int32_t *kept_pos_out, int32_t *new_len_out,
                          int32_t n_layers, int32_t kv_heads, int32_t d, int32_t cap,
                          int32_t dtype, void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * One generation step: Sec. 3.1 Eq. 1-2 and Sec. 3.2.2 Eq. 6 (the decode step
+ * of voxzip_decode_attend_score at len, next_pos), then Sec. 3.2.2 Eq. 7-9
+ * (voxzip_evict_compact of the len + 1 slots the step leaves, with next_pos +
+ * 1), in one call.  The results are those of the two calls in that order, bit
+ * for bit.  On the whole-range decode path (bf16, d = 128, at most 4 KV heads,
+ * at least 128 (layer, KV head) pairs, len + 1 <= 8224, at most 256 moved
+ * rows) the score fold and the selection run in one kernel, which takes the
+ * new scores into the selection without re-reading them.
+ *
+ *  q ... sm_scale      as for voxzip_decode_attend_score.
+ *  budget, n_sink, n_recent, kept_pos_out  as for voxzip_evict_compact; the
+ *               eviction happens when len + 1 > budget (kept_pos_out is filled
+ *               either way when given).
+ *  new_len_out  [host] receives min(len + 1, budget); the caller's next len.
+ *               The caller's next next_pos is next_pos + 1.
+ *  workspace    at least voxzip_workspace_bytes(VZ_OP_DECODE_EVICT, ...) bytes;
+ *               no initialisation needed; not shared by concurrent calls.
+ * Errors: those of the two entry points.
+ */
+VZ_API int voxzip_decode_evict(const void *q, const void *k_new, const void *v_new,
+                               void *k_cache, void *v_cache, float *score, int32_t *pos,
+                               void *out, int32_t len, int32_t next_pos, float gamma,
+                               float sm_scale, int32_t budget, int32_t n_sink,
+                               int32_t n_recent, int32_t *kept_pos_out, int32_t *new_len_out,
+                               int32_t n_layers, int32_t n_q_heads, int32_t kv_heads,
+                               int32_t d, int32_t cap, int32_t dtype, void *workspace,
+                               size_t ws_bytes, void *stream);
 
 /*
  * Workspace bytes an operation needs for the given sizes (0 on a bad op).

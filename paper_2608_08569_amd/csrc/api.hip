@@ -70,6 +70,49 @@ int check_ragged(const char* fn, int32_t L, int32_t Hkv, int32_t d, int32_t dtyp
     return VZ_OK;
 }
 
+// Arguments of a single-sequence decode step (shared by the decode entry
+// points).
+int check_decode(const char* fn, const void* q, const void* k_new, const void* v_new, const void* k_cache,
+                 const void* v_cache, const float* score, const int32_t* pos, const void* out, int32_t len,
+                 int32_t next_pos, float gamma, float sm_scale, int32_t n_layers, int32_t n_q_heads,
+                 int32_t kv_heads, int32_t d, int32_t cap, int32_t dtype) {
+    if (!q || !k_new || !v_new || !k_cache || !v_cache || !score || !pos || !out)
+        return fail(VZ_ERR_INVALID, fn, "null pointer");
+    int rc = check_common(fn, n_layers, kv_heads, d, dtype);
+    if (rc) return rc;
+    if (n_q_heads < 1 || n_q_heads % kv_heads != 0)
+        return fail(VZ_ERR_SHAPE, fn, "n_q_heads must be a positive multiple of kv_heads");
+    if (n_q_heads / kv_heads > 16) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 16 query heads per KV head");
+    if (n_q_heads > 256) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 256 query heads");
+    if (len < 0 || next_pos < 0) return fail(VZ_ERR_INVALID, fn, "negative len or next_pos");
+    if (cap < 1 || len + 1 > cap) return fail(VZ_ERR_CAPACITY, fn, "no free slot for the new token");
+    if (!(gamma >= 0.f && gamma <= 1.f)) return fail(VZ_ERR_INVALID, fn, "gamma must be in [0, 1]");
+    if (!isfinite(sm_scale)) return fail(VZ_ERR_INVALID, fn, "sm_scale must be finite");
+    return VZ_OK;
+}
+
+// Arguments of a single-sequence eviction of len slots; M receives the recent
+// window.
+int check_evict(const char* fn, int32_t len, int32_t budget, int32_t n_sink, int32_t n_recent, int32_t next_pos,
+                const int32_t* kept_pos_out, int32_t cap, int32_t& M) {
+    if (len < 0 || cap < 1) return fail(VZ_ERR_INVALID, fn, "negative len or empty cache");
+    if (len > cap) return fail(VZ_ERR_CAPACITY, fn, "len exceeds cap");
+    if (budget < 1 || n_sink < 0) return fail(VZ_ERR_INVALID, fn, "budget must be >= 1 and n_sink >= 0");
+    M = n_recent < 0 ? budget / 5 : n_recent;
+    if (static_cast<int64_t>(n_sink) + M > budget)
+        return fail(VZ_ERR_INVALID, fn, "sink and recent windows exceed the budget");
+    if (next_pos < len) return fail(VZ_ERR_INVALID, fn, "next_pos below len: positions cannot be distinct");
+    if (kept_pos_out && next_pos > (1 << 18))
+        return fail(VZ_ERR_UNSUPPORTED, fn, "kept_pos_out needs next_pos <= 262144");
+    return VZ_OK;
+}
+
+// A decode + evict workspace: the decode part, then the eviction part from
+// the next 256-byte boundary.
+size_t decode_evict_split(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap) {
+    return (vz_decode_ws_bytes(L, Hq, Hkv, d, cap, 0) + 255) / 256 * 256;
+}
+
 }  // namespace
 
 extern "C" {
@@ -99,6 +142,10 @@ size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_heads, i
         return vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap, 0);
     }
     if (op == VZ_OP_EVICT) return vz_evict_ws_bytes(n_layers, cap, 0);
+    if (op == VZ_OP_DECODE_EVICT) {
+        if (n_q_heads < 1) return 0;
+        return decode_evict_split(n_layers, n_q_heads, kv_heads, d, cap) + vz_evict_ws_bytes(n_layers, cap, 0);
+    }
     return 0;
 }
 
@@ -164,18 +211,9 @@ int voxzip_decode_attend_score(const void* q, const void* k_new, const void* v_n
                                float sm_scale, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
                                int32_t cap, int32_t dtype, void* workspace, size_t ws_bytes, void* stream) {
     static const char* fn = "voxzip_decode_attend_score";
-    if (!q || !k_new || !v_new || !k_cache || !v_cache || !score || !pos || !out)
-        return fail(VZ_ERR_INVALID, fn, "null pointer");
-    int rc = check_common(fn, n_layers, kv_heads, d, dtype);
+    int rc = check_decode(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
+                          n_layers, n_q_heads, kv_heads, d, cap, dtype);
     if (rc) return rc;
-    if (n_q_heads < 1 || n_q_heads % kv_heads != 0)
-        return fail(VZ_ERR_SHAPE, fn, "n_q_heads must be a positive multiple of kv_heads");
-    if (n_q_heads / kv_heads > 16) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 16 query heads per KV head");
-    if (n_q_heads > 256) return fail(VZ_ERR_UNSUPPORTED, fn, "more than 256 query heads");
-    if (len < 0 || next_pos < 0) return fail(VZ_ERR_INVALID, fn, "negative len or next_pos");
-    if (cap < 1 || len + 1 > cap) return fail(VZ_ERR_CAPACITY, fn, "no free slot for the new token");
-    if (!(gamma >= 0.f && gamma <= 1.f)) return fail(VZ_ERR_INVALID, fn, "gamma must be in [0, 1]");
-    if (!isfinite(sm_scale)) return fail(VZ_ERR_INVALID, fn, "sm_scale must be finite");
     const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap, 0);
     if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
     VzDecodeArgs a{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
@@ -192,15 +230,9 @@ int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* po
     if (!k_cache || !v_cache || !score || !pos || !new_len_out) return fail(VZ_ERR_INVALID, fn, "null pointer");
     int rc = check_common(fn, n_layers, kv_heads, d, dtype);
     if (rc) return rc;
-    if (len < 0 || cap < 1) return fail(VZ_ERR_INVALID, fn, "negative len or empty cache");
-    if (len > cap) return fail(VZ_ERR_CAPACITY, fn, "len exceeds cap");
-    if (budget < 1 || n_sink < 0) return fail(VZ_ERR_INVALID, fn, "budget must be >= 1 and n_sink >= 0");
-    const int32_t M = n_recent < 0 ? budget / 5 : n_recent;
-    if (static_cast<int64_t>(n_sink) + M > budget)
-        return fail(VZ_ERR_INVALID, fn, "sink and recent windows exceed the budget");
-    if (next_pos < len) return fail(VZ_ERR_INVALID, fn, "next_pos below len: positions cannot be distinct");
-    if (kept_pos_out && next_pos > (1 << 18))
-        return fail(VZ_ERR_UNSUPPORTED, fn, "kept_pos_out needs next_pos <= 262144");
+    int32_t M = 0;
+    rc = check_evict(fn, len, budget, n_sink, n_recent, next_pos, kept_pos_out, cap, M);
+    if (rc) return rc;
     const bool work = len > budget || kept_pos_out != nullptr;
     if (work) {
         const size_t need = vz_evict_ws_bytes(n_layers, cap, 0);
@@ -212,6 +244,50 @@ int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* po
                   n_layers, kv_heads, d, cap, dtype, workspace, ws_bytes, VzRagged{}, nullptr};
     hipError_t e = vz_launch_evict(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
+}
+
+int voxzip_decode_evict(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                        float* score, int32_t* pos, void* out, int32_t len, int32_t next_pos, float gamma,
+                        float sm_scale, int32_t budget, int32_t n_sink, int32_t n_recent, int32_t* kept_pos_out,
+                        int32_t* new_len_out, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
+                        int32_t cap, int32_t dtype, void* workspace, size_t ws_bytes, void* stream) {
+    static const char* fn = "voxzip_decode_evict";
+    int rc = check_decode(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
+                          n_layers, n_q_heads, kv_heads, d, cap, dtype);
+    if (rc) return rc;
+    if (!new_len_out) return fail(VZ_ERR_INVALID, fn, "null pointer");
+    // the eviction sees the cache after the append
+    const int32_t T = len + 1;
+    if (next_pos == INT32_MAX) return fail(VZ_ERR_INVALID, fn, "next_pos + 1 overflows");
+    int32_t M = 0;
+    rc = check_evict(fn, T, budget, n_sink, n_recent, next_pos + 1, kept_pos_out, cap, M);
+    if (rc) return rc;
+    const size_t split = decode_evict_split(n_layers, n_q_heads, kv_heads, d, cap);
+    const size_t need = split + vz_evict_ws_bytes(n_layers, cap, 0);
+    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    VzDecodeArgs da{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
+                    n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, split, VzRagged{}};
+    void* ews = static_cast<uint8_t*>(workspace) + split;
+    VzEvictArgs ea{k_cache, v_cache, score, pos, T, budget, n_sink, M, next_pos + 1, kept_pos_out,
+                   n_layers, kv_heads, d, cap, dtype, ews, ws_bytes - split, VzRagged{}, nullptr};
+    const bool evict = T > budget || kept_pos_out != nullptr;
+    hipError_t e;
+    if (evict && vz_decode_takes_range(da) && vz_fold_evict_ok(dtype, d, kv_heads, T, budget)) {
+        // whole-range decode without its fold launch, then fold + select in one
+        da.range_no_fold = 1;
+        e = vz_launch_decode(da, st);
+        if (e == hipSuccess)
+            e = vz_launch_fold_evict(ea, reinterpret_cast<const float*>(static_cast<uint8_t*>(workspace) +
+                                                                         vz_decode_hdr_bytes(n_layers)),
+                                     vz_range_sum_row(cap), gamma, st);
+    } else {
+        e = vz_launch_decode(da, st);
+        if (e == hipSuccess && evict) e = vz_launch_evict(ea, st);
+    }
+    if (e != hipSuccess) return hip_fail(fn, e);
+    *new_len_out = T < budget ? T : budget;
+    return VZ_OK;
 }
 
 int voxzip_fuse_spans_ragged(const void* k_in, const void* v_in, const int64_t* in_base, const int32_t* T_in,

@@ -96,4 +96,4 @@ struct FusedArgs {
 // Whole-range path (decode_range.hip): whether a single-sequence call of len
 // resident keys over L layers and Hkv KV heads takes it, and its launches.
 bool vz_decode_range_ok(int32_t len, int32_t L, int32_t Hkv);
-hipError_t vz_launch_decode_range(const vz_mfma::FusedArgs& a, int32_t Hkv, hipStream_t stream);
+hipError_t vz_launch_decode_range(const vz_mfma::FusedArgs& a, int32_t Hkv, bool fold, hipStream_t stream);

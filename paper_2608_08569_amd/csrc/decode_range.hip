@@ -375,10 +375,10 @@ __global__ __launch_bounds__(RFOLD_THREADS) void decode_range_fold_kernel(const 
 }
 
 template <int NW>
-hipError_t launch_range(const FusedArgs& a, hipStream_t stream) {
+hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
     hipLaunchKernelGGL((decode_range_kernel<NW>), dim3(NW, a.L), dim3(64 * RW), 0, stream, a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || !fold) return e;
     hipLaunchKernelGGL((decode_range_fold_kernel<NW>), dim3((a.len + RFOLD_THREADS) / RFOLD_THREADS, a.L),
                        dim3(RFOLD_THREADS), 0, stream, a);
     return hipGetLastError();
@@ -390,12 +390,14 @@ bool vz_decode_range_ok(int32_t len, int32_t L, int32_t Hkv) {
     return static_cast<int64_t>(len) + 1 <= RANGE_MAX_KEYS && static_cast<int64_t>(L) * Hkv >= RANGE_MIN_ITEMS;
 }
 
-hipError_t vz_launch_decode_range(const FusedArgs& a, int32_t Hkv, hipStream_t stream) {
+hipError_t vz_launch_decode_range(const FusedArgs& a, int32_t Hkv, bool fold, hipStream_t stream) {
     switch (Hkv) {
-        case 1: return launch_range<1>(a, stream);
-        case 2: return launch_range<2>(a, stream);
-        case 4: return launch_range<4>(a, stream);
-        case 8: return launch_range<8>(a, stream);
+        case 1: return launch_range<1>(a, fold, stream);
+        case 2: return launch_range<2>(a, fold, stream);
+        case 4: return launch_range<4>(a, fold, stream);
+        case 8: return launch_range<8>(a, fold, stream);
         default: return hipErrorInvalidValue;
     }
 }
+
+int64_t vz_range_sum_row(int64_t plane) { return range_row(plane); }

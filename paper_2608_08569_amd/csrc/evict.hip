@@ -35,6 +35,7 @@ constexpr int kInlineRows = 256;  // up to this many moved slots: K/V copied by 
 constexpr int kBitmapWords = 8192;  // kept-position bitmap: 2^18 positions
 constexpr int kLdsSlots = 16384;    // slots whose keys fit in LDS
 constexpr uint64_t kNoKey = ~0ull;  // LDS key of a slot that does not compete
+constexpr int kFoldSlots = 9 * kSel;  // slots the fused fold + select kernel takes
 
 // Block-shared state of the select kernels.  KEYS: the rank keys of the
 // layer's slots fit in LDS (kNoKey for sinks and recent slots); the
@@ -129,8 +130,9 @@ struct SelJob {
 };
 
 // LK: this layer's keys are kept in LDS (needs sh.keys and len <= kLdsSlots
-// and inline_kv).
-template <int DT, int D, bool LK, class SH>
+// and inline_kv).  READY: the caller has already filled sh.keys (and passed a
+// barrier); only with LK.
+template <int DT, int D, bool LK, class SH, bool READY = false>
 __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh) {
     using T = typename vz::Elem<DT>::T;
     constexpr int PER = vz::Elem<DT>::kPer16B;
@@ -149,7 +151,7 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh)
     const int E = len > budget ? len - budget : 0;
     const int32_t recent_from = next_pos - M;
     auto is_mid = [&](int32_t p) { return p >= n_sink && p < recent_from; };
-    if (LK) {
+    if (LK && !READY) {
         // Every slot's key in one round: up to kLdsSlots / kSel slots per
         // thread, all loads issued before any use (indexes past the end are
         // clamped, so no load sits behind a branch).  8 per thread while they
@@ -415,6 +417,86 @@ __global__ __launch_bounds__(kSel) void select_kernel(const VzEvictArgs a, int32
     select_body<DT, D, LK>(job, sh);
 }
 
+// Decode step's score fold (Sec. 3.2.2 Eq. 6) fused with the eviction that
+// follows it, one block per layer: every slot's new score is formed from the
+// old score and the KV heads' head-group sums a whole-range decode kernel
+// left in the workspace (the same additions in the same order as the
+// separate fold kernel: A = gamma A + ((S_0 + S_1) + ...) with the zero pad for
+// the new slot), stored, and turned into its rank key in LDS directly, so the
+// selection starts without re-reading the scores.  a.len and a.next_pos are
+// the eviction's (after the append).
+struct FoldIn {
+    const float* sums;  // [L][NW][row]
+    int64_t row;
+    float gamma;
+};
+
+template <int DT, int D, int NW>
+__global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, int32_t M, FoldIn f,
+                                                           int32_t* __restrict__ ws_n) {
+    using T = typename vz::Elem<DT>::T;
+    __shared__ SelShared<true> sh;
+    const int l = blockIdx.x, tid = threadIdx.x;
+    const size_t row = static_cast<size_t>(l) * a.cap;
+    float* const A = a.score + row;
+    int32_t* const P = a.pos + row;
+    const float* const S = f.sums + static_cast<size_t>(l) * NW * f.row;
+    const int len = a.len;  // keys after the append; slot len - 1 is the new one
+    const int32_t recent_from = a.next_pos - M;
+    auto fold_keys = [&](auto per_thread) {
+        constexpr int B = decltype(per_thread)::value;
+        int32_t pv[B];
+        float av[B], sv[B][NW];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {  // every load issued before any use; indexes clamped
+            const int j = min(tid + b * kSel, len - 1);
+            pv[b] = P[j];
+            av[b] = A[j];
+#pragma unroll
+            for (int g = 0; g < NW; ++g) sv[b][g] = S[g * f.row + j];
+        }
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int j = tid + b * kSel;
+            if (j < len) {
+                float acc = sv[b][0];
+#pragma unroll
+                for (int g = 1; g < NW; ++g) acc += sv[b][g];
+                const float a_new = fmaf(f.gamma, j < len - 1 ? av[b] : 0.f, acc);
+                A[j] = a_new;
+                const int32_t p = pv[b];
+                sh.keys[j] = p >= a.n_sink && p < recent_from ? vz::rank_key(a_new, p) : kNoKey;
+            }
+        }
+    };
+    // 8 slots per thread, or 9 (up to kFoldSlots): one round of loads either way
+    if (len <= 8 * kSel)
+        fold_keys(std::integral_constant<int, 8>{});
+    else
+        fold_keys(std::integral_constant<int, 9>{});
+    __syncthreads();  // keys in LDS; new scores visible to the block
+    const int E = len > a.budget ? len - a.budget : 0;
+    if (E == 0 && a.kept_pos_out == nullptr) return;
+    SelJob<T> job;
+    job.A = A;
+    job.P = P;
+    job.k0 = static_cast<T*>(a.k_cache) + row * a.Hkv * D;
+    job.v0 = static_cast<T*>(a.v_cache) + row * a.Hkv * D;
+    job.head_stride = static_cast<size_t>(a.cap) * D;
+    job.src_g = nullptr;
+    job.dst_g = nullptr;
+    job.n_out = ws_n + l;
+    job.kept = a.kept_pos_out ? a.kept_pos_out + static_cast<size_t>(l) * a.budget : nullptr;
+    job.len = len;
+    job.budget = a.budget;
+    job.n_sink = a.n_sink;
+    job.M = M;
+    job.next_pos = a.next_pos;
+    job.Hkv = a.Hkv;
+    job.inline_kv = 1;
+    select_body<DT, D, true, SelShared<true>, true>(job, sh);
+}
+
 // Status of sequence s for an eviction (VZ_OK when it can be served).
 __device__ int ragged_evict_status(const VzRagged& r, int s, int n_sink, int n_recent, bool kept) {
     const int64_t b = r.base[s];
@@ -564,6 +646,15 @@ hipError_t launch(const VzEvictArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
+template <int DT, int D, int NW>
+hipError_t launch_fold(const VzEvictArgs& a, const float* sums, int64_t row, float gamma, hipStream_t stream) {
+    EvictWs w(a.ws, a.L, a.L, a.cap);
+    const int M = a.n_recent < 0 ? a.budget / 5 : a.n_recent;
+    hipLaunchKernelGGL((fold_select_kernel<DT, D, NW>), dim3(a.L), dim3(kSel), 0, stream, a, M,
+                       FoldIn{sums, row, gamma}, w.n);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 size_t vz_evict_ws_bytes(int32_t L, int64_t plane, int32_t n_seqs) {
@@ -577,4 +668,20 @@ hipError_t vz_launch_evict(const VzEvictArgs& a, hipStream_t stream) {
     if (a.dtype == VZ_F32 && a.d == 128) return launch<VZ_F32, 128>(a, stream);
     if (a.dtype == VZ_F32 && a.d == 64) return launch<VZ_F32, 64>(a, stream);
     return hipErrorInvalidValue;
+}
+
+bool vz_fold_evict_ok(int32_t dtype, int32_t d, int32_t Hkv, int32_t len, int32_t budget) {
+    const int E = len > budget ? len - budget : 0;
+    return dtype == VZ_BF16 && d == 128 && (Hkv == 1 || Hkv == 2 || Hkv == 4) && len <= kFoldSlots &&
+           E <= kInlineRows;
+}
+
+hipError_t vz_launch_fold_evict(const VzEvictArgs& a, const float* sums, int64_t row, float gamma,
+                                hipStream_t stream) {
+    switch (a.Hkv) {
+        case 1: return launch_fold<VZ_BF16, 128, 1>(a, sums, row, gamma, stream);
+        case 2: return launch_fold<VZ_BF16, 128, 2>(a, sums, row, gamma, stream);
+        case 4: return launch_fold<VZ_BF16, 128, 4>(a, sums, row, gamma, stream);
+        default: return hipErrorInvalidValue;
+    }
 }

@@ -210,6 +210,9 @@ struct VzDecodeArgs {
     // ragged batch (rag.n > 0): len, next_pos and cap above are unused; q, out
     // are [n][L][Hq][d], k_new, v_new [n][L][Hkv][d], planes hold rag.total slots
     VzRagged rag;
+    // whole-range path only: leave the head-group sums in the workspace and
+    // skip the fold launch (a fused fold + eviction follows)
+    int32_t range_no_fold;
 };
 
 struct VzEvictArgs {
@@ -258,5 +261,15 @@ bool vz_decode_generic_ok(int64_t plane, int32_t n_seqs);
 size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_decode_generic(const VzDecodeArgs& a, hipStream_t stream);
 hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream);
+// Whole-range decode path (single sequence): whether a call takes it, and
+// where it leaves the KV heads' head-group sums ([L][Hkv][row] floats right
+// after the workspace header).
+bool vz_decode_takes_range(const VzDecodeArgs& a);
+int64_t vz_range_sum_row(int64_t plane);
+// Score fold of a whole-range decode fused with the eviction that follows
+// (bf16, d = 128, Hkv <= 4, the keys in LDS, at most 256 moved rows).
+bool vz_fold_evict_ok(int32_t dtype, int32_t d, int32_t Hkv, int32_t len, int32_t budget);
+hipError_t vz_launch_fold_evict(const VzEvictArgs& a, const float* sums, int64_t row, float gamma,
+                                hipStream_t stream);
 size_t vz_evict_ws_bytes(int32_t L, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_evict(const VzEvictArgs& a, hipStream_t stream);

@@ -257,3 +257,42 @@ def test_binding_checks_shapes_before_any_launch():
         vz._expect(Meta((2, 64), i32), (2, 64), "score", f32)
     vz._expect(Meta((2, 64), f32), (2, 64), "score", f32)
     vz._expect(None, (2, 64), "kept_pos_out", i32)
+
+
+def _step(**kw):
+    a = dict(q=FAKE, kn=FAKE, vn=FAKE, kc=FAKE, vc=FAKE, s=FAKE, p=FAKE, o=FAKE, len=10, next_pos=10,
+             gamma=0.95, scale=0.0, budget=8, n_sink=4, n_recent=-1, kept=None, nl=ctypes.byref(ctypes.c_int32()),
+             L=2, Hq=32, Hkv=4, d=128, cap=64, dtype=vz.VZ_BF16, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    return vz.lib().voxzip_decode_evict(a["q"], a["kn"], a["vn"], a["kc"], a["vc"], a["s"], a["p"], a["o"],
+                                        a["len"], a["next_pos"], a["gamma"], a["scale"], a["budget"],
+                                        a["n_sink"], a["n_recent"], a["kept"], a["nl"], a["L"], a["Hq"],
+                                        a["Hkv"], a["d"], a["cap"], a["dtype"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), vz.VZ_ERR_INVALID),
+    (dict(nl=None), vz.VZ_ERR_INVALID),
+    (dict(gamma=2.0), vz.VZ_ERR_INVALID),
+    (dict(len=64, next_pos=70), vz.VZ_ERR_CAPACITY),          # no slot for the new token
+    (dict(budget=0), vz.VZ_ERR_INVALID),
+    (dict(n_sink=4, n_recent=5), vz.VZ_ERR_INVALID),          # windows exceed the budget
+    (dict(next_pos=9), vz.VZ_ERR_INVALID),                    # next_pos below len
+    (dict(next_pos=2 ** 31 - 1), vz.VZ_ERR_INVALID),          # next_pos + 1 overflows
+    (dict(kept=FAKE, next_pos=1 << 18), vz.VZ_ERR_UNSUPPORTED),
+    (dict(d=96), vz.VZ_ERR_UNSUPPORTED),
+    (dict(ws=None, ws_bytes=1 << 20), vz.VZ_ERR_WORKSPACE),
+    (dict(ws_bytes=16), vz.VZ_ERR_WORKSPACE),                 # every case stops before any launch
+])
+def test_step_rejects(kw, code):
+    assert _step(**kw) == code
+    assert vz.lib().voxzip_last_error().decode().startswith("voxzip_decode_evict")
+
+
+def test_step_workspace_holds_both_parts():
+    for L, Hq, Hkv, d, cap in ((48, 32, 4, 128, 8194), (2, 8, 8, 64, 100)):
+        dec = vz.voxzip_workspace_bytes(vz.VZ_OP_DECODE, L, Hq, Hkv, d, cap)
+        ev = vz.voxzip_workspace_bytes(vz.VZ_OP_EVICT, L, Hq, Hkv, d, cap)
+        both = vz.voxzip_workspace_bytes(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+        assert dec + ev <= both <= dec + ev + 256
+

@@ -1,0 +1,94 @@
+"""GPU: voxzip_decode_evict (one generation step) equals voxzip_decode_attend_score
+followed by voxzip_evict_compact of the len + 1 slots it leaves, bit for bit --
+every output row, the whole cache, scores, positions, kept positions and the
+new length.  Cases cover the fused fold + select kernel of the whole-range path
+(E = 0 with kept positions, 1, 3, and 193 evictions: block minima and the
+radix select), its fallbacks (more than 256 moved rows, the chunked path, the
+generic fp32 path) and 1, 2 and 4 KV heads.  Each of the two entry points is
+checked against the oracle elsewhere."""
+import numpy as np
+import pytest
+
+import synth
+from test_gpu_range import layered_state, step_inputs
+from vzt import from_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _state(L, Hq, Hkv, d, cap, length, dtype, seed):
+    import torch
+    k, v, s, p = layered_state(seed, L, Hkv, d, cap, length, dtype, length + 9)
+    tdt = torch.float32 if dtype == synth.DT_F32 else torch.bfloat16
+    mk = lambda: dict(k=to_dev(k), v=to_dev(v), score=to_dev(s), pos=to_dev(p),
+                      out=torch.zeros(L, Hq, d, dtype=tdt, device="cuda"))
+    return mk(), mk()
+
+
+@pytest.mark.parametrize("Hq,Hkv,L,length,budget,dtype,d,kept", [
+    (32, 4, 32, 8192, 8192, synth.DT_BF16, 128, False),    # fused, E = 1
+    (32, 4, 32, 8192, 8190, synth.DT_BF16, 128, True),     # fused, E = 3, kept positions
+    (32, 4, 32, 8192, 8000, synth.DT_BF16, 128, False),    # fused, E = 193: radix select
+    (32, 4, 32, 6000, 9000, synth.DT_BF16, 128, True),     # fused, no eviction, kept positions only
+    (32, 4, 32, 6000, 9000, synth.DT_BF16, 128, False),    # decode only
+    (32, 4, 32, 8192, 7000, synth.DT_BF16, 128, False),    # E = 1193: decode, then the eviction launches
+    (16, 2, 64, 3000, 2990, synth.DT_BF16, 128, False),    # fused, 2 KV heads
+    (8, 1, 128, 1500, 1499, synth.DT_BF16, 128, True),     # fused, 1 KV head
+    (32, 4, 2, 8192, 8192, synth.DT_BF16, 128, True),      # chunked decode path (too few items)
+    (64, 8, 16, 4000, 3990, synth.DT_BF16, 128, False),    # 8 KV heads: decode, then the eviction launches
+    (8, 2, 3, 700, 650, synth.DT_F32, 64, True),           # generic decode path
+])
+def test_step_equals_decode_then_evict(Hq, Hkv, L, length, budget, dtype, d, kept):
+    import torch
+    import paper_2608_08569_amd as vz
+    cap = length + 2
+    a, b = _state(L, Hq, Hkv, d, cap, length, dtype, seed=41)
+    q, kn, vn = (to_dev(x) for x in step_inputs(synth.stream_key(41, "step", L, length), 0, L, Hq, Hkv, d, dtype))
+    next_pos = length + 9
+    kept_a = torch.full((L, budget), -1, dtype=torch.int32, device="cuda") if kept else None
+    kept_b = torch.full((L, budget), -1, dtype=torch.int32, device="cuda") if kept else None
+    ws = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+    n_a = vz.voxzip_decode_evict(q, kn, vn, a["k"], a["v"], a["score"], a["pos"], a["out"], length, next_pos,
+                                 0.95, budget, kept_pos_out=kept_a, workspace=ws)
+    ws_d = vz.workspace(vz.VZ_OP_DECODE, L, Hq, Hkv, d, cap)
+    ws_e = vz.workspace(vz.VZ_OP_EVICT, L, Hq, Hkv, d, cap)
+    vz.voxzip_decode_attend_score(q, kn, vn, b["k"], b["v"], b["score"], b["pos"], b["out"], length, next_pos,
+                                  0.95, workspace=ws_d)
+    n_b = vz.voxzip_evict_compact(b["k"], b["v"], b["score"], b["pos"], length + 1, budget, next_pos + 1,
+                                  kept_pos_out=kept_b, workspace=ws_e)
+    torch.cuda.synchronize()
+    assert n_a == n_b == min(length + 1, budget)
+    for name in ("out", "k", "v", "score", "pos"):
+        assert np.array_equal(from_dev(a[name]), from_dev(b[name])), name
+    if kept:
+        assert np.array_equal(from_dev(kept_a), from_dev(kept_b))
+    hdr = from_dev(ws[:256])
+    assert not hdr.any()  # the decode part's reserved header is left zero
+
+
+def test_steps_in_a_row():
+    """Twenty steps of the 48-layer head shape at the budget (one eviction per
+    step per layer, fused kernel), each against the two-call sequence from
+    the same state."""
+    import torch
+    import paper_2608_08569_amd as vz
+    dtype, d, L, Hq, Hkv, budget = synth.DT_BF16, 128, 48, 32, 4, 2048
+    length, cap = budget, budget + 2
+    a, b = _state(L, Hq, Hkv, d, cap, length, dtype, seed=43)
+    ws = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+    ws_d = vz.workspace(vz.VZ_OP_DECODE, L, Hq, Hkv, d, cap)
+    ws_e = vz.workspace(vz.VZ_OP_EVICT, L, Hq, Hkv, d, cap)
+    next_pos = length + 9
+    for t in range(20):
+        q, kn, vn = (to_dev(x) for x in step_inputs(synth.stream_key(43, "steps"), t, L, Hq, Hkv, d, dtype))
+        n_a = vz.voxzip_decode_evict(q, kn, vn, a["k"], a["v"], a["score"], a["pos"], a["out"], length, next_pos,
+                                     0.95, budget, workspace=ws)
+        vz.voxzip_decode_attend_score(q, kn, vn, b["k"], b["v"], b["score"], b["pos"], b["out"], length,
+                                      next_pos, 0.95, workspace=ws_d)
+        n_b = vz.voxzip_evict_compact(b["k"], b["v"], b["score"], b["pos"], length + 1, budget, next_pos + 1,
+                                      workspace=ws_e)
+        assert n_a == n_b == budget
+        torch.cuda.synchronize()
+        for name in ("out", "k", "v", "score", "pos"):
+            assert np.array_equal(from_dev(a[name]), from_dev(b[name])), (t, name)
+        length, next_pos = n_a, next_pos + 1
