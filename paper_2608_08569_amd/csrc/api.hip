@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 
 #include "vz_internal.h"
@@ -382,11 +383,11 @@ int voxzip_evict_compact_ragged(void* k_cache, void* v_cache, float* score, int3
 }  // extern "C"
 
 size_t vz_decode_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int64_t plane, int32_t n_seqs) {
-    (void)Hkv;
     (void)d;
     const size_t gen = vz_decode_generic_ws_bytes(L, Hq, plane, n_seqs);
     const size_t fused = vz_decode_fused_ws_bytes(L, Hq, plane, n_seqs);
-    return gen > fused ? gen : fused;
+    const size_t range = Hkv > 0 && Hq % Hkv == 0 ? vz_decode_range_ws_bytes(L, Hq, Hkv, plane, n_seqs) : 0;
+    return std::max(std::max(gen, fused), range);
 }
 
 hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream) {

@@ -548,7 +548,7 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
         a.n_chunks = static_cast<int32_t>((static_cast<int64_t>(v.len) + CHUNK) / CHUNK);  // of len + 1 keys
         a.nc_max = static_cast<int32_t>(chunk_rows(a.plane, 0));
     }
-    if (!RAG && vz_decode_range_ok(v.len, a.L, NW)) return vz_launch_decode_range(a, NW, !v.range_no_fold, stream);
+    if (vz_decode_range_ok(a.L, NW, RAG ? v.rag.n : 0)) return vz_launch_decode_range(a, NW, !v.range_no_fold, stream);
     hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -599,5 +599,5 @@ hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
 
 bool vz_decode_takes_range(const VzDecodeArgs& a) {
     return a.rag.n == 0 && vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.L, a.cap, 0) &&
-           vz_decode_range_ok(a.len, a.L, a.Hkv);
+           vz_decode_range_ok(a.L, a.Hkv, 0) && vz_decode_range_whole(a.len);
 }

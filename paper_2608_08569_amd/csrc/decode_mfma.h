@@ -89,11 +89,19 @@ struct FusedArgs {
     int64_t plane;          // slots per (layer, KV head) plane
     float scale_log2, gamma;
     VzRagged rag;
+    // whole-range path: a single sequence's parts (n_parts = 1: one part of
+    // every key; else parts of part_keys keys, the last one shorter), and the
+    // bounds of a ragged call's work tables (R parts, FB fold blocks)
+    int32_t n_parts, part_keys, R, FB;
 };
 
 }  // namespace vz_mfma
 
-// Whole-range path (decode_range.hip): whether a single-sequence call of len
-// resident keys over L layers and Hkv KV heads takes it, and its launches.
-bool vz_decode_range_ok(int32_t len, int32_t L, int32_t Hkv);
+// Whole-range path (decode_range.hip): whether a call over L layers, Hkv KV
+// heads and n_seqs sequences (0: a single sequence) takes it, and its
+// launches (a single sequence: a.len, a.next_pos; a ragged batch: a.rag).
+bool vz_decode_range_ok(int32_t L, int32_t Hkv, int32_t n_seqs);
 hipError_t vz_launch_decode_range(const vz_mfma::FusedArgs& a, int32_t Hkv, bool fold, hipStream_t stream);
+// Whether a single sequence of len resident keys is one part (one launch of
+// the range kernel leaving the head-group sums, then the fold).
+bool vz_decode_range_whole(int32_t len);

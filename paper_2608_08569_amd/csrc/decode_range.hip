@@ -1,6 +1,7 @@
 // Decode step (Sec. 3.1 Eq. 1-2, Sec. 3.2.2 Eq. 6), whole-range path: for a
-// single-sequence call over many (layer, KV head) items, one workgroup per
-// item streams every key, so no per-chunk partial results leave the chip.
+// call over many (layer, KV head) items, one workgroup per item streams every
+// key of a sequence (or of an 8192-key part of a longer one), so no per-chunk
+// partial results leave the chip.
 // Compiled with the max-ILP machine scheduler (per-file flag of the build):
 // the default one over-subscribes the 256 registers per lane and spills.
 #include "decode_mfma.h"
@@ -33,20 +34,152 @@ constexpr int RFULL = 8;                           // full chunks per wave
 constexpr int RNCH = RFULL + 1;                    // ... plus a last chunk of at most VT keys
 constexpr int RLDS = 5;                            // chunks whose p~ waits in LDS (the rest in registers)
 constexpr int RANGE_MAX_KEYS = RW * RFULL * CHUNK + VT;  // 8224 keys: T = B + 1 for budgets up to 8223
+constexpr int RPART = RW * RFULL * CHUNK;          // 8192: longest part of a longer sequence
 constexpr int RANGE_MIN_ITEMS = 128;               // (layer, KV head) items for the whole-range path
+constexpr int RANGE_MAX_SEQS = 1024;               // sequences of a ragged call on this path (one order block)
 constexpr int RO_STRIDE = D + 4;                   // padded LDS row of a wave's output (floats)
+constexpr int RFOLD_KEYS = 256;                    // keys per fold block; parts are multiples of it
 
-// Workspace after the header: G_sum [L][Hkv][range_row(plane)] float, the sum
-// over the KV head's query heads of p_hj for every key (rows padded to whole
-// chunks, so the last chunk of a row is written whole).
 inline __host__ __device__ int64_t range_row(int64_t plane) { return (plane + CHUNK - 1) / CHUNK * CHUNK; }
+
+// Parts of a sequence of T keys: one part when T <= RANGE_MAX_KEYS, else the
+// fewest parts of kp keys (a multiple of RFOLD_KEYS, at most RPART), the last
+// part holding the remaining T - (P - 1) kp >= 1 keys.
+__host__ __device__ inline void range_parts(int T, int& P, int& kp) {
+    if (T <= RANGE_MAX_KEYS) {
+        P = 1;
+        kp = T;
+        return;
+    }
+    const int p0 = (T + RPART - 1) / RPART;
+    kp = ((T + p0 - 1) / p0 + RFOLD_KEYS - 1) / RFOLD_KEYS * RFOLD_KEYS;
+    P = (T + kp - 1) / kp;
+}
+// Fold blocks of such a sequence (one per RFOLD_KEYS keys of each part).
+__host__ __device__ inline int range_fold_blocks(int T, int P, int kp) {
+    if (P == 1) return (T + RFOLD_KEYS - 1) / RFOLD_KEYS;
+    return (P - 1) * (kp / RFOLD_KEYS) + (T - (P - 1) * kp + RFOLD_KEYS - 1) / RFOLD_KEYS;
+}
+
+// One work item of the path: keys [k0, k1) of sequence s, part p of P.
+struct RangeItem {
+    int32_t s, p, P, kp;
+    int32_t k0, k1, len, next_pos;
+    int64_t base;  // first slot of the sequence in the planes
+    int32_t pad[6];
+};
+static_assert(sizeof(RangeItem) == 64, "one 64-byte record per item");
+
+// Workspace after the header (every array on a 256-byte boundary):
+//   sums  [L][Hkv][row] float          per key, the sum over the KV head's query
+//                                      heads of p_hj (sequences of one part;
+//                                      rows padded to whole chunks)
+//   rows  [L][Hkv][row][GMAX] half     per key and query head, p_hj relative to
+//                                      its part's max (sequences of several parts)
+//   pstat [L][Hkv][R][GMAX] float2     each part's max and sum of exp2, per head
+//   pout  [L][Hkv][R][GMAX][D] float   each part's output relative to its max
+//   ftab  [L][R][Hq] float             exp2(m_part - M) / S per part and head
+//   items [R] RangeItem                a ragged call's parts, in dispatch order
+//   fblk  [FB] int2                    a ragged call's fold blocks: (item, first key)
+// The parts' arrays exist when a sequence can have several parts (planes of
+// more than RANGE_MAX_KEYS slots), the tables in ragged calls only.  A ragged
+// call keeps its table sizes (items, fold blocks) in the header.
+struct RangeWs {
+    float* sums;
+    uint16_t* rows;
+    float2* pstat;
+    float* pout;
+    float* ftab;
+    RangeItem* items;
+    int2* fblk;
+    int32_t* counts;  // [2] in the header: items, fold blocks
+    int64_t row;
+};
+__host__ __device__ inline size_t ws_align(size_t x) { return (x + 255) / 256 * 256; }
+// Byte offsets of the arrays from the start of the workspace; returns the end.
+__host__ __device__ inline size_t range_layout(size_t hdr, int L, int NW, int Hq, int64_t plane, int R, int FB,
+                                               bool ragged, size_t off[7]) {
+    const size_t row = static_cast<size_t>(range_row(plane));
+    const size_t heads = static_cast<size_t>(L) * NW;
+    const bool parts = plane > RANGE_MAX_KEYS;
+    size_t o = ws_align(hdr);
+    off[0] = o;
+    o = ws_align(o + heads * row * sizeof(float));
+    off[1] = o;
+    if (parts) o = ws_align(o + heads * row * GMAX * sizeof(uint16_t));
+    off[2] = o;
+    if (parts) o = ws_align(o + heads * R * GMAX * sizeof(float2));
+    off[3] = o;
+    if (parts) o = ws_align(o + heads * R * GMAX * D * sizeof(float));
+    off[4] = o;
+    if (parts) o = ws_align(o + static_cast<size_t>(L) * R * Hq * sizeof(float));
+    off[5] = o;
+    if (ragged) o = ws_align(o + static_cast<size_t>(R) * sizeof(RangeItem));
+    off[6] = o;
+    if (ragged) o = ws_align(o + static_cast<size_t>(FB) * sizeof(int2));
+    return o;
+}
+template <int NW>
+__device__ __forceinline__ RangeWs range_ws(const FusedArgs& a, bool ragged) {
+    size_t off[7];
+    range_layout(a.hdr_bytes, a.L, NW, a.Hq, a.plane, a.R, a.FB, ragged, off);
+    RangeWs w;
+    w.sums = reinterpret_cast<float*>(a.ws + off[0]);
+    w.rows = reinterpret_cast<uint16_t*>(a.ws + off[1]);
+    w.pstat = reinterpret_cast<float2*>(a.ws + off[2]);
+    w.pout = reinterpret_cast<float*>(a.ws + off[3]);
+    w.ftab = reinterpret_cast<float*>(a.ws + off[4]);
+    w.items = reinterpret_cast<RangeItem*>(a.ws + off[5]);
+    w.fblk = reinterpret_cast<int2*>(a.ws + off[6]);
+    w.counts = reinterpret_cast<int32_t*>(a.ws);
+    w.row = range_row(a.plane);
+    return w;
+}
+
+// Item r of a single-sequence call (parts of a.part_keys keys).
+__device__ __forceinline__ RangeItem single_item(const FusedArgs& a, int r) {
+    RangeItem it;
+    it.s = 0;
+    it.p = r;
+    it.P = a.n_parts;
+    it.kp = a.part_keys;
+    it.k0 = r * a.part_keys;
+    it.k1 = min(a.len + 1, it.k0 + a.part_keys);
+    it.len = a.len;
+    it.next_pos = a.next_pos;
+    it.base = 0;
+    return it;
+}
 
 // Row of key r (0..CHUNK-1) in a chunk's [key][head] half-precision rows
 // (16 bytes each): bit 1 is flipped by bit 4, so that the 8 keys one write
 // instruction covers (r = c + 4 q4 + 16 hi) start on 8 distinct 4-bank groups.
 __device__ __forceinline__ int pslot(int r) { return r ^ ((r >> 3) & 2); }
 
-template <int NW>
+// Wave-uniform copy of an item (its fields feed scalar buffer descriptors).
+__device__ __forceinline__ RangeItem uniform_item(const RangeItem& x) {
+    RangeItem it;
+    it.s = __builtin_amdgcn_readfirstlane(x.s);
+    it.p = __builtin_amdgcn_readfirstlane(x.p);
+    it.P = __builtin_amdgcn_readfirstlane(x.P);
+    it.kp = __builtin_amdgcn_readfirstlane(x.kp);
+    it.k0 = __builtin_amdgcn_readfirstlane(x.k0);
+    it.k1 = __builtin_amdgcn_readfirstlane(x.k1);
+    it.len = __builtin_amdgcn_readfirstlane(x.len);
+    it.next_pos = __builtin_amdgcn_readfirstlane(x.next_pos);
+    const uint64_t b = static_cast<uint64_t>(x.base);
+    it.base = static_cast<int64_t>(
+        static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)))) |
+        (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)))) << 32));
+    return it;
+}
+
+// Grid (Hkv, L, parts): workgroup (g, l, r) takes KV head g of layer l over
+// the keys of item r.  RAG: items from the ragged call's table (dispatch
+// order longest first); else the parts of the single sequence.  SPLIT: items
+// may be parts of a longer sequence, whose statistics, outputs and per-head
+// probabilities go to the workspace for the merge and fold kernels.
+template <int NW, bool RAG, bool SPLIT>
 __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArgs a) {
     static_assert(RW * GMAX * RO_STRIDE * 4 <= RW * TILE_BYTES, "the merged outputs fit in the tile buffers");
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[RW][TILE_BYTES];
@@ -61,10 +194,20 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     const int q4 = lane >> 4, r16 = lane & 15;
     const int hi = r16 >> 3, hh = r16 & 7;
     const int Hq = a.Hq, G = Hq / NW;
-    const int g = blockIdx.x, l = blockIdx.y;
-    const int len = a.len, T = len + 1;
-    const int n_full = T / CHUNK;            // full chunks; chunk n_full holds the other T % CHUNK keys
-    const bool part = T % CHUNK != 0;
+    const int g = blockIdx.x, l = blockIdx.y, r = blockIdx.z;
+    const RangeWs rws = range_ws<NW>(a, RAG);
+    RangeItem it;
+    if constexpr (RAG) {
+        if (r >= rws.counts[0]) return;
+        it = uniform_item(rws.items[r]);
+    } else {
+        it = single_item(a, r);
+    }
+    const bool split = SPLIT && it.P > 1;
+    const int len = it.len;
+    const int NK = it.k1 - it.k0;             // keys of this item
+    const int n_full = NK / CHUNK;            // full chunks; chunk n_full holds the other NK % CHUNK keys
+    const bool part = NK % CHUNK != 0;
     const int c0 = __builtin_amdgcn_readfirstlane(w * n_full / RW);  // the wave's full chunks: [c0, c0 + my_full)
     const int my_full = __builtin_amdgcn_readfirstlane((w + 1) * n_full / RW - c0);
     const int my_chunks = my_full + (w == 0 && part ? 1 : 0);
@@ -72,23 +215,23 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     // (n_full / RW), so the partial chunk is at most its slot RFULL, and there
     // only when n_full = RW * RFULL, where the host limit leaves it <= VT keys.
     auto chunk_of = [&](int k) { return k < my_full ? c0 + k : n_full; };
-    const size_t head_base = (static_cast<size_t>(l) * NW + g) * a.plane * D;
-    uint16_t* Kh = a.k_cache + head_base;
+    const size_t seq_row = static_cast<size_t>(it.s) * a.L + l;  // (sequence, layer) row of q, out, k_new, v_new
+    const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base + it.k0) * D;
+    uint16_t* Kh = a.k_cache + head_base;  // the item's first key
     uint16_t* Vh = a.v_cache + head_base;
 
-    // Eq. (1) first: the wave whose chunks hold slot len (the partial chunk's
-    // wave 0, else the last wave) writes the new row before any of its loads,
-    // so every key is read from the cache alike.
-    if (w == (part ? 0 : RW - 1)) {
-        const uint16_t* kn = a.k_new + (static_cast<size_t>(l) * NW + g) * D;
-        const uint16_t* vn = a.v_new + (static_cast<size_t>(l) * NW + g) * D;
+    // Eq. (1) first: in the last part, the wave whose chunks hold slot len
+    // (the partial chunk's wave 0, else the last wave) writes the new row
+    // before any of its loads, so every key is read from the cache alike.
+    if (it.p == it.P - 1 && w == (part ? 0 : RW - 1)) {
+        const uint16_t* kn = a.k_new + (seq_row * NW + g) * D;
+        const uint16_t* vn = a.v_new + (seq_row * NW + g) * D;
+        const size_t at = static_cast<size_t>(len - it.k0) * D;
         if (lane < 16)
-            *reinterpret_cast<uint4*>(Kh + static_cast<size_t>(len) * D + 8 * lane) =
-                *reinterpret_cast<const uint4*>(kn + 8 * lane);
+            *reinterpret_cast<uint4*>(Kh + at + 8 * lane) = *reinterpret_cast<const uint4*>(kn + 8 * lane);
         else if (lane < 32)
-            *reinterpret_cast<uint4*>(Vh + static_cast<size_t>(len) * D + 8 * (lane - 16)) =
-                *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
-        if (g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + len] = a.next_pos;
+            *reinterpret_cast<uint4*>(Vh + at + 8 * (lane - 16)) = *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
+        if (g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
         __threadfence_block();
     }
 
@@ -101,7 +244,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     auto load_tile = [&](int k, int j, uint4 (&dst)[8]) {
         const bool live = k < my_chunks;
         const int c = live ? chunk_of(k) : 0;
-        const int nk = live ? min(CHUNK, T - c * CHUNK) : 0;
+        const int nk = live ? min(CHUNK, NK - c * CHUNK) : 0;
         const int u = j & 3;
         const int rows = nk - VT * u > 0 ? nk - VT * u : 0;
         const uint16_t* base = (j < 4 ? Kh : Vh) + (static_cast<size_t>(c) * CHUNK + VT * u) * D;
@@ -125,7 +268,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     uint4 qv[KSTEPS];  // B operand: Q^T, column r16 = query head (zero past G)
     {
         const int hq = r16 < G ? r16 : 0;
-        const uint16_t* qrow = a.q + (static_cast<size_t>(l) * Hq + g * G + hq) * D + 8 * q4;
+        const uint16_t* qrow = a.q + (seq_row * Hq + g * G + hq) * D + 8 * q4;
 #pragma unroll
         for (int s = 0; s < KSTEPS; ++s) {
             const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * s);
@@ -149,7 +292,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     for (int k = 0; k < RNCH; ++k) {
         if (k < my_chunks) {
         const int c = chunk_of(k);
-        const int nk = min(CHUNK, T - c * CHUNK);
+        const int nk = min(CHUNK, NK - c * CHUNK);
         // ---- pass 1: logits S^T = K Q^T ----
         float sp[PAIRS][4];
 #pragma unroll
@@ -273,8 +416,12 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         const float2 st = s_stat[v][hh];
         S = fmaf(st.y, st.x == -INFINITY ? 0.f : exp2f(st.x - M), S);
     }
-    const float inv_S = 1.0f / S;
+    // a part of a longer sequence keeps its output and p~ relative to its own
+    // max; the merge kernel applies the sequence's statistics
+    const float inv_S = split ? 1.f : 1.0f / S;
     if (w == 0 && q4 == 0 && hi == 0) s_MS[hh] = make_float2(M, inv_S);  // read after the next barrier
+    const size_t part_row = (static_cast<size_t>(l) * NW + g) * a.R + r;  // (layer, KV head, item) of pstat, pout
+    if (split && w == 0 && q4 == 0 && hi == 0 && hh < G) rws.pstat[part_row * GMAX + hh] = make_float2(M, S);
 
     // ---- output rows: the waves' outputs, rescaled, summed in wave order ----
     float* const s_o = reinterpret_cast<float*>(&s_tile[0][0]);  // [RW][GMAX][RO_STRIDE]
@@ -292,7 +439,10 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         float o = 0.f;
 #pragma unroll
         for (int v = 0; v < RW; ++v) o += s_o[(v * GMAX + h) * RO_STRIDE + ch];
-        a.out[(static_cast<size_t>(l) * Hq + g * G + h) * D + ch] = vz::f32_to_bf16(o);
+        if (split)
+            rws.pout[(part_row * GMAX + h) * D + ch] = o;
+        else
+            a.out[(seq_row * Hq + g * G + h) * D + ch] = vz::f32_to_bf16(o);
     }
 
     // ---- each key's sum over this KV head's query heads of p_hj ----
@@ -304,7 +454,9 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     // operations of a wave complete in order: no barrier between a wave's own
     // writes and reads.)
     __syncthreads();  // the output merge has read the tile buffers; s_MS is written
-    float* const gsum = reinterpret_cast<float*>(a.ws + a.hdr_bytes) + (static_cast<size_t>(l) * NW + g) * range_row(a.plane);
+    const size_t key0 = (static_cast<size_t>(l) * NW + g) * rws.row + it.base + it.k0;  // the item's first key
+    float* const gsum = rws.sums + key0;
+    uint16_t* const prow = rws.rows + key0 * GMAX;
     // factor table, in place of the reference maxima: f[k][h]
     for (int e = lane; e < RNCH * GMAX; e += 64) {
         const int k = e / GMAX, h = e - k * GMAX;
@@ -324,10 +476,10 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
 #pragma unroll
             for (int i = 2; i < 2 * PAIRS; ++i) pk[i] = 0;  // keys past the cache: p~ = 0
 #pragma unroll
-            for (int r = 0; r < RFULL - RLDS; ++r)  // register slots: fixed indexes, wave-uniform choice
-                if (k == RLDS + r) {
+            for (int x = 0; x < RFULL - RLDS; ++x)  // register slots: fixed indexes, wave-uniform choice
+                if (k == RLDS + x) {
 #pragma unroll
-                    for (int i = 0; i < 2 * PAIRS; ++i) pk[i] = pst[r][i];
+                    for (int i = 0; i < 2 * PAIRS; ++i) pk[i] = pst[x][i];
                 }
 #pragma unroll
             for (int u = 0; u < PAIRS; ++u)
@@ -340,18 +492,41 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         const float4 fa = *reinterpret_cast<const float4*>(&s_mref[w][k][0]);
         const float4 fb = *reinterpret_cast<const float4*>(&s_mref[w][k][4]);
         const float fk[GMAX] = {fa.x, fa.y, fa.z, fa.w, fb.x, fb.y, fb.z, fb.w};
-        float y[2];
+        const int kk = chunk_of(k) * CHUNK + 2 * lane;  // the lane's first key in the item
+        if (split) {
+            // each key's row of p~ f_h (relative to the part's max), half precision
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const uint4 r = *reinterpret_cast<const uint4*>(rows + pslot(2 * lane + e) * GMAX);
-            const uint32_t wd[4] = {r.x, r.y, r.z, r.w};
-            float acc = 0.f;
+            for (int e = 0; e < 2; ++e) {
+                const uint4 rw = *reinterpret_cast<const uint4*>(rows + pslot(2 * lane + e) * GMAX);
+                const uint32_t wd[4] = {rw.x, rw.y, rw.z, rw.w};
+                uint32_t ow[4];
 #pragma unroll
-            for (int h = 0; h < GMAX; ++h)
-                acc = fmaf(f16_to_f32(static_cast<uint16_t>(wd[h >> 1] >> (16 * (h & 1)))), fk[h], acc);
-            y[e] = acc;
+                for (int i = 0; i < 4; ++i)
+                    ow[i] = pack_f16x2(f16_to_f32(static_cast<uint16_t>(wd[i])) * fk[2 * i],
+                                       f16_to_f32(static_cast<uint16_t>(wd[i] >> 16)) * fk[2 * i + 1]);
+                if (kk + e < NK)
+                    *reinterpret_cast<uint4*>(prow + static_cast<size_t>(kk + e) * GMAX) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+            }
+        } else {
+            float y[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const uint4 rw = *reinterpret_cast<const uint4*>(rows + pslot(2 * lane + e) * GMAX);
+                const uint32_t wd[4] = {rw.x, rw.y, rw.z, rw.w};
+                float acc = 0.f;
+#pragma unroll
+                for (int h = 0; h < GMAX; ++h)
+                    acc = fmaf(f16_to_f32(static_cast<uint16_t>(wd[h >> 1] >> (16 * (h & 1)))), fk[h], acc);
+                y[e] = acc;
+            }
+            if constexpr (RAG) {
+                // slots past the item belong to the next sequence: masked
+                if (kk < NK) gsum[kk] = y[0];
+                if (kk + 1 < NK) gsum[kk + 1] = y[1];
+            } else {
+                *reinterpret_cast<float2*>(gsum + kk) = make_float2(y[0], y[1]);
+            }
         }
-        *reinterpret_cast<float2*>(gsum + chunk_of(k) * CHUNK + 2 * lane) = make_float2(y[0], y[1]);
     }
 }
 
@@ -374,9 +549,226 @@ __global__ __launch_bounds__(RFOLD_THREADS) void decode_range_fold_kernel(const 
     if (static_cast<int>(blockIdx.x) * RFOLD_THREADS + static_cast<int>(threadIdx.x) <= len) *sc = fmaf(a.gamma, a_old, acc);
 }
 
+// Merge of a sequence in parts, one block per (sequence, layer) at its first
+// part: per query head the sequence's max M and sum S from the parts' pairs,
+// each part's factor exp2(m_part - M) / S (kept for the fold), and the output
+// row, the parts' outputs times their factors.
+constexpr int RMERGE_THREADS = 256;
+template <int NW, bool RAG>
+__global__ __launch_bounds__(RMERGE_THREADS) void range_merge_kernel(const FusedArgs a) {
+    const int r = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    const RangeWs rws = range_ws<NW>(a, RAG);
+    RangeItem it;
+    if constexpr (RAG) {
+        if (r >= rws.counts[0]) return;
+        it = rws.items[r];
+    } else {
+        it = single_item(a, r);
+    }
+    if (it.P == 1 || it.p != 0) return;
+    const int Hq = a.Hq, G = Hq / NW, P = it.P;
+    for (int h = t; h < Hq; h += RMERGE_THREADS) {
+        const int g = h / G, hg = h - g * G;
+        const float2* ps = rws.pstat + ((static_cast<size_t>(l) * NW + g) * a.R + r) * GMAX + hg;
+        float M = -INFINITY;
+        for (int p = 0; p < P; ++p) M = fmaxf(M, ps[static_cast<size_t>(p) * GMAX].x);
+        float S = 0.f;
+        for (int p = 0; p < P; ++p) {
+            const float2 x = ps[static_cast<size_t>(p) * GMAX];
+            S = fmaf(x.y, exp2f(x.x - M), S);
+        }
+        const float inv_S = 1.0f / S;
+        for (int p = 0; p < P; ++p)
+            rws.ftab[(static_cast<size_t>(l) * a.R + r + p) * Hq + h] = exp2f(ps[static_cast<size_t>(p) * GMAX].x - M) * inv_S;
+    }
+    __syncthreads();  // the block's factors are visible to the block
+    for (int e = t; e < Hq * D; e += RMERGE_THREADS) {
+        const int h = e / D, ch = e - h * D;
+        const int g = h / G, hg = h - g * G;
+        const float* po = rws.pout + (((static_cast<size_t>(l) * NW + g) * a.R + r) * GMAX + hg) * D + ch;
+        const float* f = rws.ftab + (static_cast<size_t>(l) * a.R + r) * Hq + h;
+        float o = 0.f;
+        for (int p = 0; p < P; ++p) o = fmaf(po[static_cast<size_t>(p) * GMAX * D], f[static_cast<size_t>(p) * Hq], o);
+        a.out[((static_cast<size_t>(it.s) * a.L + l) * Hq + h) * D + ch] = vz::f32_to_bf16(o);
+    }
+}
+
+// Fold kernel of a ragged call or of a sequence in parts, one block of
+// RFOLD_KEYS threads per fold block (keys of one item), thread = key: Eq. (6)
+// from the KV heads' sums added in head order (a sequence of one part, the
+// same arithmetic as the single-part fold kernel), or from each key's
+// per-head rows and its part's factors.
+template <int NW, bool RAG>
+__global__ __launch_bounds__(RFOLD_KEYS) void range_fold_parts_kernel(const FusedArgs a) {
+    __shared__ float s_f[NW * GMAX];
+    const int b = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    const RangeWs rws = range_ws<NW>(a, RAG);
+    int r, j0;
+    RangeItem it;
+    if constexpr (RAG) {
+        if (b >= rws.counts[1]) return;
+        const int2 e = rws.fblk[b];
+        r = e.x;
+        j0 = e.y;
+        it = rws.items[r];
+    } else {
+        const int bpp = a.part_keys / RFOLD_KEYS;
+        r = min(b / bpp, a.n_parts - 1);
+        j0 = r * a.part_keys + (b - r * bpp) * RFOLD_KEYS;
+        it = single_item(a, r);
+        if (j0 >= it.k1) return;
+    }
+    const int len = it.len;
+    const int jj = j0 + t;
+    const int j = min(jj, it.k1 - 1);  // clamped: every load in bounds, the store masked
+    const size_t slot = static_cast<size_t>(it.base) + j;
+    float* const sc = a.score + static_cast<size_t>(l) * a.plane + slot;
+    const float a_ld = *sc;
+    float acc;
+    if (it.P == 1) {
+        const float* gs = rws.sums + static_cast<size_t>(l) * NW * rws.row + slot;
+        acc = gs[0];
+#pragma unroll
+        for (int g = 1; g < NW; ++g) acc += gs[g * rws.row];
+    } else {
+        const int Hq = a.Hq, G = Hq / NW;
+        uint4 rw[NW];
+#pragma unroll
+        for (int g = 0; g < NW; ++g)
+            rw[g] = *reinterpret_cast<const uint4*>(rws.rows + ((static_cast<size_t>(l) * NW + g) * rws.row + slot) * GMAX);
+        if (t < NW * GMAX) {
+            const int g = t / GMAX, hg = t - g * GMAX;
+            s_f[t] = hg < G ? rws.ftab[(static_cast<size_t>(l) * a.R + r) * Hq + g * G + hg] : 0.f;
+        }
+        __syncthreads();
+        acc = 0.f;
+#pragma unroll
+        for (int g = 0; g < NW; ++g) {
+            const uint32_t wd[4] = {rw[g].x, rw[g].y, rw[g].z, rw[g].w};
+#pragma unroll
+            for (int h = 0; h < GMAX; ++h)
+                acc = fmaf(f16_to_f32(static_cast<uint16_t>(wd[h >> 1] >> (16 * (h & 1)))), s_f[g * GMAX + h], acc);
+        }
+    }
+    const float a_old = j < len ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
+    if (jj < it.k1) *sc = fmaf(a.gamma, a_old, acc);
+}
+
+// Work order of a ragged call, one block: every served sequence's parts,
+// those of the longest parts first (ties: the smaller sequence index), so
+// that the workgroups starting last are the short ones; the fold blocks of
+// each part; each sequence's status.  A sequence that cannot be served, or
+// whose parts would not fit the tables (sequences overlapping in the planes),
+// is skipped and its status says why.
+constexpr int ORDER_THREADS = RANGE_MAX_SEQS;
+template <int NW>
+__global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedArgs a) {
+    __shared__ int s_kp[ORDER_THREADS], s_P[ORDER_THREADS], s_F[ORDER_THREADS];
+    __shared__ int s_seq[ORDER_THREADS], s_fb[ORDER_THREADS], s_r0[ORDER_THREADS];
+    __shared__ int s_n[3];  // sequences served, items, fold blocks
+    const RangeWs rws = range_ws<NW>(a, true);
+    const int n = a.rag.n, t = threadIdx.x;
+    if (t < 3) s_n[t] = 0;
+    int st = VZ_OK, T = 0, P = 0, kp = 0, F = 0;
+    if (t < n) {
+        st = vz::ragged_decode_status(a.rag, t);
+        if (st == VZ_OK) {
+            T = a.rag.len[t] + 1;
+            range_parts(T, P, kp);
+            F = range_fold_blocks(T, P, kp);
+        }
+        s_kp[t] = kp;
+        s_P[t] = P;
+        s_F[t] = F;
+    }
+    __syncthreads();
+    // position among the served sequences, first item, first fold block
+    int q = 0, r0 = 0, fb0 = 0;
+    if (P > 0) {
+        for (int u = 0; u < n; ++u) {
+            const int ku = s_kp[u];
+            if (ku > kp || (ku == kp && u < t)) {
+                ++q;
+                r0 += s_P[u];
+                fb0 += s_F[u];
+            }
+        }
+    }
+    // a sequence that does not fit pushes every later one out as well, so the
+    // served ones hold positions 0 .. served - 1
+    const bool fits = P > 0 && r0 + P <= a.R && fb0 + F <= a.FB;
+    if (P > 0 && !fits) st = VZ_ERR_CAPACITY;
+    if (t < n && a.rag.status) a.rag.status[t] = st;
+    if (fits) {
+        s_seq[q] = t;
+        s_fb[q] = fb0;
+        s_r0[q] = r0;
+        atomicAdd(&s_n[0], 1);
+        atomicMax(&s_n[1], r0 + P);
+        atomicMax(&s_n[2], fb0 + F);
+        RangeItem it{};
+        it.s = t;
+        it.P = P;
+        it.kp = kp;
+        it.len = T - 1;
+        it.next_pos = a.rag.next_pos[t];
+        it.base = a.rag.base[t];
+        for (int p = 0; p < P; ++p) {
+            it.p = p;
+            it.k0 = p * kp;
+            it.k1 = min(T, (p + 1) * kp);
+            rws.items[r0 + p] = it;
+        }
+    }
+    __syncthreads();
+    const int served = s_n[0], n_fold = s_n[2];
+    for (int b = t; b < n_fold; b += ORDER_THREADS) {
+        int lo = 0, hi = served - 1;  // the last position whose first fold block is <= b
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_fb[mid] <= b) lo = mid;
+            else hi = mid - 1;
+        }
+        const int u = s_seq[lo], o = b - s_fb[lo];
+        const int Pu = s_P[u], kpu = s_kp[u];
+        const int bpp = Pu == 1 ? 1 : kpu / RFOLD_KEYS;
+        const int p = Pu == 1 ? 0 : min(o / bpp, Pu - 1);
+        rws.fblk[b] = make_int2(s_r0[lo] + p, p * kpu + (o - p * bpp) * RFOLD_KEYS);
+    }
+    if (t == 0) {
+        rws.counts[0] = s_n[1];
+        rws.counts[1] = n_fold;
+    }
+}
+
+// Item and fold-block bounds of a ragged call over `total` slots: a sequence
+// of T keys has at most T / RPART + 1 parts and T / RFOLD_KEYS + (parts) fold
+// blocks, and the sequences' keys add up to at most `total`.
+int32_t ragged_items_bound(int32_t n_seqs, int64_t total) {
+    return static_cast<int32_t>(n_seqs + (total + RPART - 1) / RPART);
+}
+int32_t ragged_fold_bound(int32_t n_seqs, int64_t total) {
+    return static_cast<int32_t>((total + RFOLD_KEYS - 1) / RFOLD_KEYS + ragged_items_bound(n_seqs, total));
+}
+
 template <int NW>
 hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
-    hipLaunchKernelGGL((decode_range_kernel<NW>), dim3(NW, a.L), dim3(64 * RW), 0, stream, a);
+    if (a.rag.n > 0) {
+        hipLaunchKernelGGL((range_order_kernel<NW>), dim3(1), dim3(ORDER_THREADS), 0, stream, a);
+        hipLaunchKernelGGL((decode_range_kernel<NW, true, true>), dim3(NW, a.L, a.R), dim3(64 * RW), 0, stream, a);
+        hipLaunchKernelGGL((range_merge_kernel<NW, true>), dim3(a.R, a.L), dim3(RMERGE_THREADS), 0, stream, a);
+        hipLaunchKernelGGL((range_fold_parts_kernel<NW, true>), dim3(a.FB, a.L), dim3(RFOLD_KEYS), 0, stream, a);
+        return hipGetLastError();
+    }
+    if (a.n_parts > 1) {
+        hipLaunchKernelGGL((decode_range_kernel<NW, false, true>), dim3(NW, a.L, a.n_parts), dim3(64 * RW), 0, stream, a);
+        hipLaunchKernelGGL((range_merge_kernel<NW, false>), dim3(1, a.L), dim3(RMERGE_THREADS), 0, stream, a);
+        hipLaunchKernelGGL((range_fold_parts_kernel<NW, false>),
+                           dim3(range_fold_blocks(a.len + 1, a.n_parts, a.part_keys), a.L), dim3(RFOLD_KEYS), 0,
+                           stream, a);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((decode_range_kernel<NW, false, false>), dim3(NW, a.L, 1), dim3(64 * RW), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !fold) return e;
     hipLaunchKernelGGL((decode_range_fold_kernel<NW>), dim3((a.len + RFOLD_THREADS) / RFOLD_THREADS, a.L),
@@ -386,11 +778,21 @@ hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
 
 }  // namespace
 
-bool vz_decode_range_ok(int32_t len, int32_t L, int32_t Hkv) {
-    return static_cast<int64_t>(len) + 1 <= RANGE_MAX_KEYS && static_cast<int64_t>(L) * Hkv >= RANGE_MIN_ITEMS;
+bool vz_decode_range_ok(int32_t L, int32_t Hkv, int32_t n_seqs) {
+    return static_cast<int64_t>(L) * Hkv >= RANGE_MIN_ITEMS && n_seqs <= RANGE_MAX_SEQS;
 }
 
-hipError_t vz_launch_decode_range(const FusedArgs& a, int32_t Hkv, bool fold, hipStream_t stream) {
+hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, bool fold, hipStream_t stream) {
+    FusedArgs a = a0;
+    if (a.rag.n > 0) {
+        a.R = ragged_items_bound(a.rag.n, a.plane);
+        a.FB = ragged_fold_bound(a.rag.n, a.plane);
+    } else {
+        range_parts(a.len + 1, a.n_parts, a.part_keys);
+        a.R = a.n_parts;
+        a.FB = 0;
+        if (a.n_parts > 65535) return hipErrorInvalidValue;  // grid z
+    }
     switch (Hkv) {
         case 1: return launch_range<1>(a, fold, stream);
         case 2: return launch_range<2>(a, fold, stream);
@@ -398,6 +800,16 @@ hipError_t vz_launch_decode_range(const FusedArgs& a, int32_t Hkv, bool fold, hi
         case 8: return launch_range<8>(a, fold, stream);
         default: return hipErrorInvalidValue;
     }
+}
+
+bool vz_decode_range_whole(int32_t len) { return static_cast<int64_t>(len) + 1 <= RANGE_MAX_KEYS; }
+
+size_t vz_decode_range_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int64_t plane, int32_t n_seqs) {
+    size_t off[7];
+    const bool rag = n_seqs > 0;
+    const int R = rag ? ragged_items_bound(n_seqs, plane) : static_cast<int>((plane + RPART - 1) / RPART);
+    const int FB = rag ? ragged_fold_bound(n_seqs, plane) : 0;
+    return range_layout(vz_decode_hdr_bytes(L), L, Hkv, Hq, plane, R, FB, rag, off);
 }
 
 int64_t vz_range_sum_row(int64_t plane) { return range_row(plane); }

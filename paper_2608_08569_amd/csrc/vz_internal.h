@@ -266,6 +266,8 @@ hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream);
 // after the workspace header).
 bool vz_decode_takes_range(const VzDecodeArgs& a);
 int64_t vz_range_sum_row(int64_t plane);
+// Workspace of the whole-range path (single sequence or ragged batch).
+size_t vz_decode_range_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int64_t plane, int32_t n_seqs);
 // Score fold of a whole-range decode fused with the eviction that follows
 // (bf16, d = 128, Hkv <= 4, the keys in LDS, at most 256 moved rows).
 bool vz_fold_evict_ok(int32_t dtype, int32_t d, int32_t Hkv, int32_t len, int32_t budget);

@@ -1,8 +1,10 @@
 """The decode loop on the ragged entry points (paper_2608_08569_amd.loop):
 one step captured as a HIP graph and replayed per token gives the same bits
 as the same steps launched eagerly, in the all-layer and the per-layer mode,
-with the eviction schedule; per-layer calls give the same bits as one call
-over all layers; the first step matches the oracle."""
+with the eviction schedule (also over 32 layers, where the one call takes the
+whole-range path: order, range, merge and fold kernels in the graph);
+per-layer calls give the same bits as one call over all layers; the first
+step matches the oracle."""
 import numpy as np
 import pytest
 
@@ -19,7 +21,7 @@ INTERVAL = 2
 STEPS = 8
 
 
-def _loop():
+def _loop(L=L):
     import torch
     from paper_2608_08569_amd.loop import DecodeLoop
     offs = [synth.offsets_from_lengths(synth.spans_geometric(synth.stream_key(5, "loop", i), T, 0.25, 32))
@@ -40,7 +42,7 @@ def _loop():
     return lp
 
 
-def _inputs(step):
+def _inputs(step, L=L):
     n = len(T_IN)
     key = synth.stream_key(6, "loop-step", step)
     mk = lambda tag, shape: synth.as_storage(
@@ -59,10 +61,10 @@ def _layer_major(a):
     return np.ascontiguousarray(np.transpose(a, (1, 0, 2, 3))[:, :, None])
 
 
-@pytest.mark.parametrize("per_layer", [False, True])
-def test_graph_replay_matches_eager_steps(per_layer):
+@pytest.mark.parametrize("per_layer,L", [(False, L), (True, L), (False, 32)])
+def test_graph_replay_matches_eager_steps(per_layer, L):
     import torch
-    eager, graph = _loop(), _loop()
+    eager, graph = _loop(L), _loop(L)
     n = len(T_IN)
     if per_layer:
         qb = torch.zeros(L, n, 1, HQ, D, dtype=torch.bfloat16, device="cuda")
@@ -84,7 +86,7 @@ def test_graph_replay_matches_eager_steps(per_layer):
     for a, b in zip(_state(eager), _state(graph)):
         assert np.array_equal(a, b), "capture changed the state"
     for step in range(STEPS):
-        q, k, v = _inputs(step)
+        q, k, v = _inputs(step, L)
         if per_layer:
             q, k, v = _layer_major(q), _layer_major(k), _layer_major(v)
         qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)

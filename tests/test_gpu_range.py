@@ -1,10 +1,11 @@
 """GPU parity of the whole-range decode path: single-sequence bf16 calls with at
-least 128 (layer, KV head) items and at most 8224 keys, where one workgroup
-streams every key of a (layer, KV head).  State-synced against the fp64 oracle
-(every layer for short caches, sampled layers for long ones); the cases cover
-caches shorter than one chunk per wave, ragged tails, the 8224-key maximum
-(8 chunks per wave and one 32-key tile) and the first length past it (chunked
-path), 1 to 8 query heads per KV head."""
+least 128 (layer, KV head) items, where one workgroup streams every key of a
+(layer, KV head), or of one part of at most 8192 keys when the cache holds
+more than 8224.  State-synced against the fp64 oracle (every layer for short
+caches, sampled layers for long ones); the cases cover caches shorter than one
+chunk per wave, ragged tails, the 8224-key maximum of one part (8 chunks per
+wave and one 32-key tile), caches of 2 and 3 parts, 1 to 8 query heads per KV
+head."""
 import numpy as np
 import pytest
 
@@ -60,18 +61,28 @@ def test_whole_range_short_all_layers(length):
     run_case(32, 4, 32, length, steps=2)
 
 
-@pytest.mark.parametrize("length", [4095, 8191, 8192, 8222, 8223, 8224])
+@pytest.mark.parametrize("length", [4095, 8191, 8192, 8222, 8223])
 def test_whole_range_long_sampled_layers(length):
     """8 full chunks per wave (8191 -> 8192 keys), one more key or tile on
-    the last wave (up to 8223 -> 8224 keys, the whole-range maximum) and the
-    first cache past it (chunked path); layers 0, 13 and 31."""
+    the last wave (up to 8223 -> 8224 keys, the one-part maximum); layers 0,
+    13 and 31."""
     run_case(32, 4, 32, length, steps=1, layers=[0, 13, 31])
 
 
+@pytest.mark.parametrize("length", [8224, 9215, 12000, 16384, 20000])
+def test_whole_range_parts_sampled_layers(length):
+    """Caches in parts: 8225 keys (the first past one part: 2 parts of 4352
+    and 3873 keys), 12001 (2 parts), 16385 and 20001 (3 parts), two steps
+    (the second one key longer); layers 0, 13 and 31."""
+    run_case(32, 4, 32, length, steps=2, layers=[0, 13, 31])
+
+
 @pytest.mark.parametrize("Hq,Hkv,L,length", [(16, 4, 32, 3000), (64, 8, 16, 5000), (8, 1, 128, 2000),
-                                             (12, 2, 64, 777), (24, 4, 32, 8192)])
+                                             (12, 2, 64, 777), (24, 4, 32, 8192), (64, 8, 16, 9000),
+                                             (8, 1, 128, 8500), (12, 2, 64, 10000)])
 def test_whole_range_head_groups(Hq, Hkv, L, length):
-    """4, 8, 6 and 3 query heads per KV head, and 1, 2 or 8 KV heads."""
+    """4, 8, 6 and 3 query heads per KV head, and 1, 2 or 8 KV heads; one
+    part, or two parts for the longer caches."""
     run_case(Hq, Hkv, L, length, steps=1, layers=[0, L // 2, L - 1])
 
 

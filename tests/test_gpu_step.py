@@ -32,6 +32,7 @@ def _state(L, Hq, Hkv, d, cap, length, dtype, seed):
     (32, 4, 32, 6000, 9000, synth.DT_BF16, 128, True),     # fused, no eviction, kept positions only
     (32, 4, 32, 6000, 9000, synth.DT_BF16, 128, False),    # decode only
     (32, 4, 32, 8192, 7000, synth.DT_BF16, 128, False),    # E = 1193: decode, then the eviction launches
+    (32, 4, 32, 8224, 8200, synth.DT_BF16, 128, True),     # decode in two parts, then the eviction launches
     (16, 2, 64, 3000, 2990, synth.DT_BF16, 128, False),    # fused, 2 KV heads
     (8, 1, 128, 1500, 1499, synth.DT_BF16, 128, True),     # fused, 1 KV head
     (32, 4, 2, 8192, 8192, synth.DT_BF16, 128, True),      # chunked decode path (too few items)
