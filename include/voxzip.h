@@ -299,7 +299,7 @@ VZ_API int voxzip_fuse_spans_ragged(const void *k_in, const void *v_in, const in
  * the same data.
  * Per-sequence errors (status): VZ_ERR_INVALID (negative len or next_pos, a
  * range outside the planes), VZ_ERR_CAPACITY (len + 1 > cap, or sequences that
- * overlap so that their chunks exceed the planes).
+ * overlap in the planes so that their work exceeds the bound the planes set).
  * Returned errors: as voxzip_decode_attend_score, plus VZ_ERR_SHAPE for
  * n_seqs or total out of range.
  */
