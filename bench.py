@@ -590,8 +590,10 @@ def main():
         "path_gbps": path_bytes / elapsed / 1e9,
         "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
         "step_us_steady": float(np.mean(step_ms)) * 1e3,
+        "step_us_median": float(np.median(step_ms)) * 1e3,
         "step_gbps_steady": step_bytes_ss / (float(np.mean(step_ms)) * 1e-3) / 1e9,
         "decode_us_mean": dec_mean_s * 1e6,
+        "decode_us_median": float(np.median(dec_ms)) * 1e3,
         "fuse_ms_mean": float(np.mean(fuse_ms)),
         "fuse_gbps": fuse_bytes / (float(np.mean(fuse_ms)) * 1e-3) / 1e9,
         "roofline": {

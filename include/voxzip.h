@@ -44,7 +44,7 @@ extern "C" {
 #define VZ_ERR_CAPACITY -3    /* the cache or an output has no room */
 #define VZ_ERR_UNSUPPORTED -4 /* dtype / head size / group size this build does not serve */
 #define VZ_ERR_HIP -5         /* a HIP call failed; voxzip_last_error() has its text */
-#define VZ_ERR_WORKSPACE -6   /* workspace missing or smaller than voxzip_workspace_bytes() */
+#define VZ_ERR_WORKSPACE -6   /* workspace missing, not 16-byte aligned, or smaller than voxzip_workspace_bytes() */
 
 /* Element types. */
 #define VZ_F32 0
@@ -142,7 +142,8 @@ VZ_API int voxzip_fuse_spans(const void *k_in, const void *v_in, int32_t T_in,
  *  gamma        decay in [0, 1] (1 = plain accumulation).
  *  sm_scale     softmax scale; <= 0 selects 1 / sqrt(d).
  *  workspace    device scratch of at least voxzip_workspace_bytes(VZ_OP_DECODE,
- *               ...) bytes (per-chunk partial results); it needs no
+ *               ...) bytes (per-chunk partial results), 16-byte aligned (as
+ *               every workspace of this library); it needs no
  *               initialisation.  One workspace must not be used by two calls
  *               that can run at the same time.
  * The caller advances len and next_pos by one after the call.

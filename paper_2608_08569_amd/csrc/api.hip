@@ -108,6 +108,12 @@ int check_evict(const char* fn, int32_t len, int32_t budget, int32_t n_sink, int
     return VZ_OK;
 }
 
+// A workspace is usable when present, 16-byte aligned (its arrays are read
+// and written with 16-byte accesses) and large enough.
+bool ws_ok(const void* ws, size_t ws_bytes, size_t need) {
+    return ws != nullptr && (reinterpret_cast<uintptr_t>(ws) & 15u) == 0 && ws_bytes >= need;
+}
+
 // A decode + evict workspace: the decode part, then the eviction part from
 // the next 256-byte boundary.
 size_t decode_evict_split(int32_t L, int32_t Hq, int32_t Hkv, int32_t d, int32_t cap) {
@@ -216,7 +222,7 @@ int voxzip_decode_attend_score(const void* q, const void* k_new, const void* v_n
                           n_layers, n_q_heads, kv_heads, d, cap, dtype);
     if (rc) return rc;
     const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap, 0);
-    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     VzDecodeArgs a{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
                    n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, ws_bytes, VzRagged{}};
     hipError_t e = vz_launch_decode(a, static_cast<hipStream_t>(stream));
@@ -237,7 +243,7 @@ int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* po
     const bool work = len > budget || kept_pos_out != nullptr;
     if (work) {
         const size_t need = vz_evict_ws_bytes(n_layers, cap, 0);
-        if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+        if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     }
     *new_len_out = len < budget ? len : budget;
     if (!work) return VZ_OK;
@@ -265,7 +271,7 @@ int voxzip_decode_evict(const void* q, const void* k_new, const void* v_new, voi
     if (rc) return rc;
     const size_t split = decode_evict_split(n_layers, n_q_heads, kv_heads, d, cap);
     const size_t need = split + vz_evict_ws_bytes(n_layers, cap, 0);
-    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     hipStream_t st = static_cast<hipStream_t>(stream);
     VzDecodeArgs da{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
                     n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, split, VzRagged{}};
@@ -349,7 +355,7 @@ int voxzip_decode_attend_score_ragged(const void* q, const void* k_new, const vo
     if (!(gamma >= 0.f && gamma <= 1.f)) return fail(VZ_ERR_INVALID, fn, "gamma must be in [0, 1]");
     if (!isfinite(sm_scale)) return fail(VZ_ERR_INVALID, fn, "sm_scale must be finite");
     const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, total, n_seqs);
-    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     VzRagged rg{seq_base, cap, len, next_pos, nullptr, status, n_seqs, total};
     VzDecodeArgs a{q,  k_new, v_new, k_cache, v_cache, score, pos,   out,       0,        0,  gamma, sm_scale,
                    n_layers, n_q_heads, kv_heads, d, 0, dtype, workspace, ws_bytes, rg};
@@ -372,7 +378,7 @@ int voxzip_evict_compact_ragged(void* k_cache, void* v_cache, float* score, int3
     if (new_len_out && overlaps(new_len_out, 4 * static_cast<size_t>(n_seqs), len, 4 * static_cast<size_t>(n_seqs)))
         return fail(VZ_ERR_INVALID, fn, "new_len_out must not overlap len");
     const size_t need = vz_evict_ws_bytes(n_layers, total, n_seqs);
-    if (!workspace || ws_bytes < need) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing or too small");
+    if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     VzRagged rg{seq_base, cap, len, next_pos, budget, status, n_seqs, total};
     VzEvictArgs a{k_cache, v_cache, score, pos, 0, 0, n_sink, n_recent, 0, kept_pos_out,
                   n_layers, kv_heads, d, 0, dtype, workspace, ws_bytes, rg, new_len_out};

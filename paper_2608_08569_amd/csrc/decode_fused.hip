@@ -447,11 +447,11 @@ __device__ float2 merge_output_row(const FusedArgs& a, const Partials& part, int
 // the output row, the layer's (max, 1 / sum) of the head for the fold kernel
 // and, in a ragged call, the sequence's status.
 template <bool RAG>
-__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedArgs a) {
-    const int h = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+__device__ void output_block(const FusedArgs& a, int h, int l, int s_arg, bool store_layer) {
+    const int t = threadIdx.x;
     int s = 0, first = 0, n_chunks = a.n_chunks;
     if constexpr (RAG) {
-        s = blockIdx.z;
+        s = s_arg;
         const int st = vz::ragged_decode_status(a.rag, s);
         first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
         n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
@@ -461,7 +461,12 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedA
     }
     Partials part(a.ws, a.hdr_bytes, a.L, a.nc_max, a.Hq);
     const float2 stats = merge_output_row(a, part, h, l, s, first, n_chunks);
-    if (t == 0) part.layer[(static_cast<size_t>(s) * a.L + l) * a.Hq + h] = stats;
+    if (store_layer && t == 0) part.layer[(static_cast<size_t>(s) * a.L + l) * a.Hq + h] = stats;
+}
+
+template <bool RAG>
+__global__ __launch_bounds__(OUT_THREADS) void decode_output_kernel(const FusedArgs a) {
+    output_block<RAG>(a, blockIdx.x, blockIdx.y, blockIdx.z, true);
 }
 
 // Fold kernel, one block of CHUNK threads per (chunk, layer), thread = key:
@@ -509,6 +514,110 @@ __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
     if (t < nk) *sc = fmaf(a.gamma, a_old, acc);
 }
 
+// Output merge and score fold in one launch, for calls whose sequences have
+// few chunks (planes of at most FINISH_MAX_CHUNKS chunks).  Blocks
+// [0, n_chunks) of a layer are fold blocks: one per chunk, each forms every
+// head's layer statistics itself from its sequence's chunk pairs, with the
+// output kernel's arithmetic and order (the same bits), then folds its
+// chunk's keys as the fold kernel does.  The blocks after them are the output
+// kernel's blocks, one per (head, sequence), run beside the fold blocks.  The
+// recomputation reads n_chunks x Hq pairs per fold block, cheap while chunks
+// are few.
+constexpr int FINISH_MAX_CHUNKS = 128;
+constexpr int FINISH_MAX_HEADS = 8 * GMAX;  // Hq <= Hkv * GMAX with Hkv <= 8
+template <bool RAG>
+__global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedArgs a) {
+    __shared__ float s_gm[FINISH_MAX_HEADS * OUT_ROWS], s_gl[FINISH_MAX_HEADS * OUT_ROWS];
+    __shared__ float2 s_stat[FINISH_MAX_HEADS];
+    __shared__ float s_f[FOLD_HEADS];
+    const int t = threadIdx.x, l = blockIdx.y, Hq = a.Hq;
+    if (static_cast<int>(blockIdx.x) >= a.n_chunks) {
+        const int ob = static_cast<int>(blockIdx.x) - a.n_chunks;
+        output_block<RAG>(a, ob % Hq, l, ob / Hq, false);
+        return;
+    }
+    SeqItem it;
+    int c;
+    if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) return;
+    const ConstPartials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
+    const size_t row0 = static_cast<size_t>(l) * a.nc_max + it.first;
+    const int nch = it.n_chunks;
+    // Loads first, all independent of one another: the chunk pairs of the
+    // statistics (thread t: (head, row group) pairs t, t + OUT_THREADS, ...,
+    // up to FINISH_GROUP_CHUNKS chunks each, indexes clamped), the fold's p~
+    // of the first FOLD_HEADS heads, its chunk's own pairs and the scores.
+    constexpr int FINISH_GROUP_CHUNKS = FINISH_MAX_CHUNKS / OUT_ROWS;
+    constexpr int FINISH_PAIRS = FINISH_MAX_HEADS * OUT_ROWS / OUT_THREADS;
+    float2 stv[FINISH_PAIRS][FINISH_GROUP_CHUNKS];
+#pragma unroll
+    for (int u = 0; u < FINISH_PAIRS; ++u) {
+        const int pi = min(t + u * OUT_THREADS, Hq * OUT_ROWS - 1);
+        const int h = pi / OUT_ROWS, rg = pi - h * OUT_ROWS;
+#pragma unroll
+        for (int k = 0; k < FINISH_GROUP_CHUNKS; ++k)
+            stv[u][k] = part.ml[(row0 + min(rg + k * OUT_ROWS, nch - 1)) * Hq + h];
+    }
+    const int len = it.len, T = len + 1;
+    const int nk = chunk_keys(c, T);
+    const int tk = t < CHUNK ? t : 0;
+    const int j = chunk_begin(c) + (tk < nk ? tk : 0);
+    float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
+    const float a_ld = *sc;
+    const size_t cbase = (row0 + c) * Hq;
+    const uint16_t* pp = part.p + cbase * CHUNK + tk;
+    uint16_t pr[FOLD_HEADS];
+#pragma unroll
+    for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(q, Hq - 1) * CHUNK];
+    const float m_own = part.ml[cbase + min(t % FOLD_HEADS, Hq - 1)].x;
+
+    // the layer statistics of every head: row group rg of head h takes
+    // chunks rg, rg + OUT_ROWS, ... with a running max, then the groups merge
+#pragma unroll
+    for (int u = 0; u < FINISH_PAIRS; ++u) {
+        const int pi = t + u * OUT_THREADS;
+        if (pi < Hq * OUT_ROWS) {
+            const int rg = pi % OUT_ROWS;
+            float M = -INFINITY, S = 0.f;
+#pragma unroll
+            for (int k = 0; k < FINISH_GROUP_CHUNKS; ++k) {
+                if (rg + k * OUT_ROWS >= nch) break;
+                const float2 st = stv[u][k];
+                if (st.x > M) {
+                    S *= exp2f(M - st.x);
+                    M = st.x;
+                }
+                S = fmaf(exp2f(st.x - M), st.y, S);
+            }
+            s_gm[pi] = M;
+            s_gl[pi] = S;
+        }
+    }
+    __syncthreads();
+    if (t < Hq) s_stat[t] = combine_rows(&s_gm[t * OUT_ROWS], &s_gl[t * OUT_ROWS], 1);
+    __syncthreads();
+
+    // Eq. (6) for the chunk's keys (threads below CHUNK), as the fold kernel
+    const float a_old = (tk < nk && j < len) ? a_ld : 0.f;
+    float acc = 0.f;
+    for (int hb = 0; hb < Hq; hb += FOLD_HEADS) {
+        if (hb > 0) {
+#pragma unroll
+            for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(hb + q, Hq - 1) * CHUNK];
+        }
+        if (t < FOLD_HEADS && hb + t < Hq) {
+            const float2 gl = s_stat[hb + t];
+            const float m_c = hb == 0 ? m_own : part.ml[cbase + hb + t].x;
+            s_f[t] = exp2f(m_c - gl.x) * gl.y;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < FOLD_HEADS; ++q)
+            if (hb + q < Hq) acc = fmaf(f16_to_f32(pr[q]), s_f[q], acc);
+        __syncthreads();
+    }
+    if (t < CHUNK && t < nk) *sc = fmaf(a.gamma, a_old, acc);
+}
+
 // Chunk rows of the partials per layer: ceil(plane / CHUNK) for a single
 // sequence; for a ragged call ceil(plane / CHUNK) + n_seqs, a bound on the
 // sum of ceil((len[s] + 1) / CHUNK) over sequences that lie inside the planes
@@ -552,6 +661,11 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
     hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if ((a.plane + CHUNK - 1) / CHUNK <= FINISH_MAX_CHUNKS) {
+        hipLaunchKernelGGL((decode_finish_kernel<RAG>), dim3(a.n_chunks + a.Hq * seqs, a.L), dim3(OUT_THREADS), 0,
+                           stream, a);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((decode_output_kernel<RAG>), dim3(a.Hq, a.L, seqs), dim3(OUT_THREADS), 0, stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

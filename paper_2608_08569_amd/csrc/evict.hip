@@ -53,6 +53,8 @@ struct SelShared {
     int32_t ev[kSmallE];     // slots of the evicted keys found by the rounds (keys in LDS only)
     int32_t holes[kSmallE];  // those below the budget, ascending
     int nm;
+    float pre_a[kSmallE];    // fused fold: new score and position of the slots at or past the budget
+    int32_t pre_p[kSmallE];
     int32_t src[kInlineRows], dst[kInlineRows];  // move lists (keys in LDS only)
     uint64_t keys[KEYS ? kLdsSlots : 1];
     uint32_t own_bitmap[KEYS ? 1 : kBitmapWords];
@@ -132,8 +134,10 @@ struct SelJob {
 // LK: this layer's keys are kept in LDS (needs sh.keys and len <= kLdsSlots
 // and inline_kv).  READY: the caller has already filled sh.keys (and passed a
 // barrier); only with LK.
-template <int DT, int D, bool LK, class SH, bool READY = false>
-__device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh) {
+// move_fn(n_moves, src, dst), when given, may perform the moves itself (and
+// return true) instead of the copies below.
+template <int DT, int D, bool LK, class SH, bool READY = false, class MoveFn = std::nullptr_t>
+__device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh, MoveFn move_fn = nullptr) {
     using T = typename vz::Elem<DT>::T;
     constexpr int PER = vz::Elem<DT>::kPer16B;
     constexpr int CH = D / PER;
@@ -338,13 +342,16 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh)
         __syncthreads();
     }
 
-    for (int r = tid; r < n_moves; r += kSel) {
-        const int s = src[r], d = dst[r];
-        A[d] = A[s];
-        P[d] = P[s];
-    }
+    bool moved = false;
+    if constexpr (!std::is_same<MoveFn, std::nullptr_t>::value) moved = move_fn(n_moves, src, dst);
+    if (!moved)
+        for (int r = tid; r < n_moves; r += kSel) {
+            const int s = src[r], d = dst[r];
+            A[d] = A[s];
+            P[d] = P[s];
+        }
     if (tid == 0) *job.n_out = (LK || job.inline_kv) ? 0 : n_moves;
-    if (LK || job.inline_kv) {
+    if (!moved && (LK || job.inline_kv)) {
         const int total = n_moves * Hkv * 2 * CH;
         for (int i = tid; i < total; i += kSel) {
             const int c = i % CH;
@@ -443,6 +450,32 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
     const float* const S = f.sums + static_cast<size_t>(l) * NW * f.row;
     const int len = a.len;  // keys after the append; slot len - 1 is the new one
     const int32_t recent_from = a.next_pos - M;
+    T* const k0 = static_cast<T*>(a.k_cache) + row * a.Hkv * D;
+    T* const v0 = static_cast<T*>(a.v_cache) + row * a.Hkv * D;
+    const size_t head_stride = static_cast<size_t>(a.cap) * D;
+    // With at most kSmallE evictions the movers are among the E slots at or
+    // past the budget: their K/V rows are loaded now, beside the fold's loads
+    // (one 16-byte piece per thread), and their new score and position kept
+    // in LDS, so that the moves after the selection are stores only.
+    constexpr int PER = vz::Elem<DT>::kPer16B;
+    constexpr int CH = D / PER;
+    const int E = len > a.budget ? len - a.budget : 0;
+    const bool pre = E > 0 && E <= kSmallE;
+    const int n_pre = pre ? E * NW * 2 * CH : 0;
+    static_assert(kSmallE * NW * 2 * CH <= kSel, "one piece per thread");
+    uint4 piece = make_uint4(0, 0, 0, 0);
+    int piece_slot = -1;
+    T* piece_base = nullptr;
+    if (tid < n_pre) {
+        const int c = tid % CH;
+        int t = tid / CH;
+        const int which = t & 1;
+        t >>= 1;
+        const int h = t % NW;
+        piece_slot = a.budget + t / NW;
+        piece_base = (which ? v0 : k0) + h * head_stride + c * PER;
+        piece = *reinterpret_cast<const uint4*>(piece_base + static_cast<size_t>(piece_slot) * D);
+    }
     auto fold_keys = [&](auto per_thread) {
         constexpr int B = decltype(per_thread)::value;
         int32_t pv[B];
@@ -466,6 +499,10 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
                 A[j] = a_new;
                 const int32_t p = pv[b];
                 sh.keys[j] = p >= a.n_sink && p < recent_from ? vz::rank_key(a_new, p) : kNoKey;
+                if (pre && j >= a.budget) {
+                    sh.pre_a[j - a.budget] = a_new;
+                    sh.pre_p[j - a.budget] = p;
+                }
             }
         }
     };
@@ -475,14 +512,13 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
     else
         fold_keys(std::integral_constant<int, 9>{});
     __syncthreads();  // keys in LDS; new scores visible to the block
-    const int E = len > a.budget ? len - a.budget : 0;
     if (E == 0 && a.kept_pos_out == nullptr) return;
     SelJob<T> job;
     job.A = A;
     job.P = P;
-    job.k0 = static_cast<T*>(a.k_cache) + row * a.Hkv * D;
-    job.v0 = static_cast<T*>(a.v_cache) + row * a.Hkv * D;
-    job.head_stride = static_cast<size_t>(a.cap) * D;
+    job.k0 = k0;
+    job.v0 = v0;
+    job.head_stride = head_stride;
     job.src_g = nullptr;
     job.dst_g = nullptr;
     job.n_out = ws_n + l;
@@ -494,7 +530,21 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
     job.next_pos = a.next_pos;
     job.Hkv = a.Hkv;
     job.inline_kv = 1;
-    select_body<DT, D, true, SelShared<true>, true>(job, sh);
+    // the moves from the prefetched rows (pairs in LDS, at most kSmallE)
+    auto move_pre = [&](int n_moves, const int32_t* src, const int32_t* dst) -> bool {
+        if (!pre) return false;
+        if (tid < n_moves) {
+            const int sj = src[tid] - a.budget;
+            A[dst[tid]] = sh.pre_a[sj];
+            P[dst[tid]] = sh.pre_p[sj];
+        }
+        if (piece_slot >= 0)
+            for (int r = 0; r < n_moves; ++r)
+                if (src[r] == piece_slot)
+                    *reinterpret_cast<uint4*>(piece_base + static_cast<size_t>(dst[r]) * D) = piece;
+        return true;
+    };
+    select_body<DT, D, true, SelShared<true>, true>(job, sh, move_pre);
 }
 
 // Status of sequence s for an eviction (VZ_OK when it can be served).

@@ -11,6 +11,7 @@ import paper_2608_08569_amd as vz
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: every case fails validation first
+MISALIGNED = ctypes.c_void_p(0x10008)  # a workspace address off the 16-byte grid
 
 
 def _declared():
@@ -65,6 +66,7 @@ def _decode(**kw):
     (dict(dtype=7), vz.VZ_ERR_UNSUPPORTED),
     (dict(ws=None), vz.VZ_ERR_WORKSPACE),
     (dict(ws_bytes=16), vz.VZ_ERR_WORKSPACE),
+    (dict(ws=MISALIGNED), vz.VZ_ERR_WORKSPACE),   # 8 bytes past a 16-byte boundary
 ])
 def test_decode_rejects(kw, code):
     assert _decode(**kw) == code
@@ -93,6 +95,7 @@ def _evict(**kw):
     (dict(kept=FAKE, next_pos=(1 << 18) + 1), vz.VZ_ERR_UNSUPPORTED),
     (dict(ws=None), vz.VZ_ERR_WORKSPACE),
     (dict(ws_bytes=8), vz.VZ_ERR_WORKSPACE),
+    (dict(ws=MISALIGNED), vz.VZ_ERR_WORKSPACE),
 ])
 def test_evict_rejects(kw, code):
     rc, _ = _evict(**kw)
@@ -174,6 +177,7 @@ def _decode_ragged(**kw):
     (dict(d=96), vz.VZ_ERR_UNSUPPORTED),
     (dict(L=70000), vz.VZ_ERR_UNSUPPORTED),
     (dict(ws_bytes=64), vz.VZ_ERR_WORKSPACE),
+    (dict(ws=MISALIGNED), vz.VZ_ERR_WORKSPACE),
 ])
 def test_decode_ragged_rejects(kw, code):
     assert _decode_ragged(**kw) == code
@@ -283,6 +287,7 @@ def _step(**kw):
     (dict(d=96), vz.VZ_ERR_UNSUPPORTED),
     (dict(ws=None, ws_bytes=1 << 20), vz.VZ_ERR_WORKSPACE),
     (dict(ws_bytes=16), vz.VZ_ERR_WORKSPACE),                 # every case stops before any launch
+    (dict(ws=MISALIGNED, ws_bytes=1 << 30), vz.VZ_ERR_WORKSPACE),
 ])
 def test_step_rejects(kw, code):
     assert _step(**kw) == code

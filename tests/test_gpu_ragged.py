@@ -137,6 +137,14 @@ def test_ragged_decode_generic_path(dtype, d, Hq, Hkv):
     _run_decode_case(dtype, d, Hq, Hkv, LENS[::2] + [300], seed=7 + Hq)
 
 
+def test_ragged_decode_finishing_launches_agree():
+    """Planes of more than 128 chunks take the output and fold kernels, smaller
+    ones one finishing kernel that forms the layer statistics itself: the
+    300-key sequence's ragged call (a 17,300-slot plane, two launches) gives
+    the bits of its single call (one launch), and so does the long one."""
+    _run_decode_case(synth.DT_BF16, 128, 32, 4, [300, 17000], steps=1, seed=12)
+
+
 def test_ragged_decode_one_sequence_and_gamma_edges():
     _run_decode_case(synth.DT_BF16, 128, 32, 4, [2000], steps=1, gamma=1.0, seed=3)
     _run_decode_case(synth.DT_BF16, 128, 32, 4, [9, 300], steps=1, gamma=0.0, seed=4)
