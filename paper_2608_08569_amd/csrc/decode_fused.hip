@@ -42,6 +42,7 @@ namespace {
 using namespace vz_mfma;
 
 constexpr int ATTEND_WG_PER_CU = 4;  // resident attend workgroups per CU (128 VGPRs)
+constexpr int ATTEND_DEEP_MAX_ITEMS = 512;  // attend grids this small keep four tiles in flight per wave
 constexpr size_t kHeaderBytes = 256;  // decode workspace header (unused by this path)
 
 // Per-chunk partial results in the workspace, after the header:
@@ -111,8 +112,13 @@ __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem
     return true;
 }
 
-template <int NW, bool RAG>
-__global__ __launch_bounds__(64 * NW, ATTEND_WG_PER_CU) void decode_attend_kernel(const FusedArgs a) {
+// DEPTH: K/V tiles in flight per wave.  1 keeps the registers within four
+// resident workgroups per CU; 4 (the K tiles at once, each V tile issued as
+// its K slot frees) shortens the chain of dependent loads for grids too small
+// to fill the GPU, where occupancy does not matter.  The arithmetic is the
+// same, so are the bits.
+template <int NW, bool RAG, int DEPTH>
+__global__ __launch_bounds__(64 * NW, DEPTH == 1 ? ATTEND_WG_PER_CU : 1) void decode_attend_kernel(const FusedArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][TILE_BYTES];
     const int tid = threadIdx.x;
     // wave-uniform values go through readfirstlane so that addresses built
@@ -181,18 +187,22 @@ __global__ __launch_bounds__(64 * NW, ATTEND_WG_PER_CU) void decode_attend_kerne
     const uint16_t* const kc = Kh + static_cast<size_t>(k_begin) * D;
     const uint16_t* const vc = Vh + static_cast<size_t>(k_begin) * D;
     const int lane_off = q4 * (D * 2) + 16 * r16;
-    uint4 stg[8];
-    auto load_tile = [&](const uint16_t* base, int u) {
+    // tile tt: K tiles 0 .. PAIRS - 1, then V tiles; held in slot tt % DEPTH
+    uint4 stg[DEPTH][8];
+    auto load_tile = [&](int tt) {
+        const uint16_t* base = tt < PAIRS ? kc : vc;
+        const int u = tt % PAIRS;
         const int rows = nk - VT * u > 0 ? nk - VT * u : 0;
         const __amdgpu_buffer_rsrc_t rs =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base) + VT * u * D, 0, rows * D * 2, kBufferDword3);
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
             const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lane_off + 4 * m * (D * 2), 0, 0);
-            __builtin_memcpy(&stg[m], &v, 16);
+            __builtin_memcpy(&stg[tt % DEPTH][m], &v, 16);
         }
     };
-    load_tile(kc, 0);
+#pragma unroll
+    for (int tt = 0; tt < DEPTH; ++tt) load_tile(tt);
 
     // Per-lane LDS bases.  Stores: lane (q4, r16) writes 16-byte column r16 of
     // row 4m + q4 in instruction m.  K reads (A operand of S^T = K Q^T): row
@@ -223,9 +233,8 @@ __global__ __launch_bounds__(64 * NW, ATTEND_WG_PER_CU) void decode_attend_kerne
 #pragma unroll
     for (int u = 0; u < PAIRS; ++u) {
 #pragma unroll
-        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(kw + 4 * KSTRIDE * m) = stg[m];
-        if (u + 1 < PAIRS) load_tile(kc, u + 1);
-        else load_tile(vc, 0);  // the first V tile follows the last K tile
+        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(kw + 4 * KSTRIDE * m) = stg[u % DEPTH][m];
+        if (u + DEPTH < 2 * PAIRS) load_tile(u + DEPTH);  // the V tiles follow the K tiles
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
         f32x4 acc[2];
 #pragma unroll
@@ -280,8 +289,8 @@ __global__ __launch_bounds__(64 * NW, ATTEND_WG_PER_CU) void decode_attend_kerne
 #pragma unroll
     for (int u = 0; u < PAIRS; ++u) {
 #pragma unroll
-        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vw + 4 * VSTRIDE * m) = stg[m];
-        if (u + 1 < PAIRS) load_tile(vc, u + 1);
+        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vw + 4 * VSTRIDE * m) = stg[(PAIRS + u) % DEPTH][m];
+        if (PAIRS + u + DEPTH < 2 * PAIRS) load_tile(PAIRS + u + DEPTH);
         // B operand P^T: column = head r16 (columns >= G feed output columns
         // that are never stored), k-slots 8 q4 + i -> keys 32u + 4 q4 + i (i < 4)
         // and 32u + 16 + 4 q4 + i - 4 (i >= 4): the even tile is in place, the
@@ -658,7 +667,12 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
         a.nc_max = static_cast<int32_t>(chunk_rows(a.plane, 0));
     }
     if (vz_decode_range_ok(a.L, NW, RAG ? v.rag.n : 0)) return vz_launch_decode_range(a, NW, !v.range_no_fold, stream);
-    hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
+    // grids of at most two workgroups per CU: four tiles in flight per wave
+    // (all eight measured slower: their registers spill into the AGPRs)
+    if (static_cast<int64_t>(a.L) * a.n_chunks <= ATTEND_DEEP_MAX_ITEMS)
+        hipLaunchKernelGGL((decode_attend_kernel<NW, RAG, PAIRS>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
+    else
+        hipLaunchKernelGGL((decode_attend_kernel<NW, RAG, 1>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((a.plane + CHUNK - 1) / CHUNK <= FINISH_MAX_CHUNKS) {

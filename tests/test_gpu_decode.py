@@ -174,6 +174,32 @@ def test_many_chunks_per_layer():
     synced_step(g, q, kn, vn, 0.95)
 
 
+def test_small_and_large_chunked_grids_agree():
+    """A chunked call over 20 layers (32 chunks each: 640 workgroups, one tile
+    in flight per wave) and one-layer calls of the same data (32 workgroups,
+    four tiles in flight) give the same bits; the first layer also against
+    the oracle."""
+    dtype, L, Hq, Hkv, d, length = synth.DT_BF16, 20, 32, 4, 128, 4000
+    k, v, s, p = synth.random_state(14, L, Hkv, d, length + 2, length, dtype, next_pos=length + 9)
+    key = synth.stream_key(14, "grids")
+    mk = lambda tag, shape: synth.as_storage(synth.normal_f32(synth.stream_key(key, tag), int(np.prod(shape)))
+                                             .reshape(shape), dtype)
+    q, kn, vn = mk("q", (L, Hq, d)), mk("k", (L, Hkv, d)), mk("v", (L, Hkv, d))
+    g = GpuCache(L, Hq, Hkv, d, length + 2, dtype)
+    g.load(k, v, s, p, length, length + 9)
+    ref_s, _ = synced_step(g, q, kn, vn, 0.95, layers=[0])
+    out_all = from_dev(g.out)
+    K_all, V_all, S_all, P_all = g.snapshot()
+    for l in range(L):
+        h = GpuCache(1, Hq, Hkv, d, length + 2, dtype)
+        h.load(k[l:l + 1], v[l:l + 1], s[l:l + 1], p[l:l + 1], length, length + 9)
+        h.step(to_dev(q[l:l + 1]), to_dev(kn[l:l + 1]), to_dev(vn[l:l + 1]), 0.95)
+        Kh, Vh, Sh, Ph = h.snapshot()
+        assert np.array_equal(from_dev(h.out)[0], out_all[l]), f"layer {l} output"
+        assert np.array_equal(Sh[0], S_all[l]) and np.array_equal(Ph[0], P_all[l])
+        assert np.array_equal(Kh[0], K_all[l]) and np.array_equal(Vh[0], V_all[l])
+
+
 def test_deterministic_bits():
     """Two identical steps from the same state give identical bits."""
     w = synth.workload("layer")
