@@ -36,7 +36,7 @@ constexpr int RLDS = 5;                            // chunks whose p~ waits in L
 constexpr int RANGE_MAX_KEYS = RW * RFULL * CHUNK + VT;  // 8224 keys: T = B + 1 for budgets up to 8223
 constexpr int RPART = RW * RFULL * CHUNK;          // 8192: longest part of a longer sequence
 constexpr int RANGE_MIN_ITEMS = 128;               // (layer, KV head) items for the whole-range path
-constexpr int RANGE_MAX_SEQS = 1024;               // sequences of a ragged call on this path (one order block)
+constexpr int RANGE_MAX_SEQS = 1024;               // sequences a ragged call ranks longest first (one order block)
 constexpr int RO_STRIDE = D + 4;                   // padded LDS row of a wave's output (floats)
 constexpr int RFOLD_KEYS = 256;                    // keys per fold block; parts are multiples of it
 
@@ -659,8 +659,83 @@ __global__ __launch_bounds__(RFOLD_KEYS) void range_fold_parts_kernel(const Fuse
 // that the workgroups starting last are the short ones; the fold blocks of
 // each part; each sequence's status.  A sequence that cannot be served, or
 // whose parts would not fit the tables (sequences overlapping in the planes),
-// is skipped and its status says why.
+// is skipped and its status says why.  Batches of more than ORDER_THREADS
+// sequences keep the sequence order instead (each thread a run of
+// sequences, a block scan for the first item and fold block of each run).
 constexpr int ORDER_THREADS = RANGE_MAX_SEQS;
+
+// Parts and fold blocks of sequence s (0 when it cannot be served).
+__device__ __forceinline__ void order_seq(const FusedArgs& a, int s, int& st, int& T, int& P, int& kp, int& F) {
+    T = P = kp = F = 0;
+    st = vz::ragged_decode_status(a.rag, s);
+    if (st == VZ_OK) {
+        T = a.rag.len[s] + 1;
+        range_parts(T, P, kp);
+        F = range_fold_blocks(T, P, kp);
+    }
+}
+
+// Items r0 .. r0 + P - 1 and fold blocks fb0 .. fb0 + F - 1 of sequence s.
+__device__ void order_write(const FusedArgs& a, const RangeWs& rws, int s, int T, int P, int kp, int r0, int fb0,
+                            bool fold_entries) {
+    RangeItem it{};
+    it.s = s;
+    it.P = P;
+    it.kp = kp;
+    it.len = T - 1;
+    it.next_pos = a.rag.next_pos[s];
+    it.base = a.rag.base[s];
+    int fb = fb0;
+    for (int p = 0; p < P; ++p) {
+        it.p = p;
+        it.k0 = p * kp;
+        it.k1 = min(T, (p + 1) * kp);
+        rws.items[r0 + p] = it;
+        if (fold_entries)
+            for (int j0 = it.k0; j0 < it.k1; j0 += RFOLD_KEYS) rws.fblk[fb++] = make_int2(r0 + p, j0);
+    }
+}
+
+template <int NW>
+__device__ void order_in_sequence_order(const FusedArgs& a, const RangeWs& rws, int* s_a, int* s_b, int* s_n) {
+    const int n = a.rag.n, t = threadIdx.x;
+    const int per = (n + ORDER_THREADS - 1) / ORDER_THREADS;
+    const int s0 = min(t * per, n), s1 = min(s0 + per, n);
+    int sumP = 0, sumF = 0;
+    for (int s = s0; s < s1; ++s) {
+        int st, T, P, kp, F;
+        order_seq(a, s, st, T, P, kp, F);
+        sumP += P;
+        sumF += F;
+    }
+    // exclusive block scan of the runs' items and fold blocks
+    s_a[t] = sumP;
+    s_b[t] = sumF;
+    __syncthreads();
+    for (int o = 1; o < ORDER_THREADS; o <<= 1) {
+        const int xa = t >= o ? s_a[t - o] : 0, xb = t >= o ? s_b[t - o] : 0;
+        __syncthreads();
+        s_a[t] += xa;
+        s_b[t] += xb;
+        __syncthreads();
+    }
+    int r = s_a[t] - sumP, fb = s_b[t] - sumF;
+    for (int s = s0; s < s1; ++s) {
+        int st, T, P, kp, F;
+        order_seq(a, s, st, T, P, kp, F);
+        const bool fits = P > 0 && r + P <= a.R && fb + F <= a.FB;
+        if (P > 0 && !fits) st = VZ_ERR_CAPACITY;
+        if (a.rag.status) a.rag.status[s] = st;
+        if (fits) {
+            order_write(a, rws, s, T, P, kp, r, fb, true);
+            atomicMax(&s_n[1], r + P);
+            atomicMax(&s_n[2], fb + F);
+        }
+        r += P;
+        fb += F;
+    }
+}
+
 template <int NW>
 __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedArgs a) {
     __shared__ int s_kp[ORDER_THREADS], s_P[ORDER_THREADS], s_F[ORDER_THREADS];
@@ -669,14 +744,19 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
     const RangeWs rws = range_ws<NW>(a, true);
     const int n = a.rag.n, t = threadIdx.x;
     if (t < 3) s_n[t] = 0;
+    if (n > ORDER_THREADS) {
+        __syncthreads();
+        order_in_sequence_order<NW>(a, rws, s_kp, s_P, s_n);
+        __syncthreads();
+        if (t == 0) {
+            rws.counts[0] = s_n[1];
+            rws.counts[1] = s_n[2];
+        }
+        return;
+    }
     int st = VZ_OK, T = 0, P = 0, kp = 0, F = 0;
     if (t < n) {
-        st = vz::ragged_decode_status(a.rag, t);
-        if (st == VZ_OK) {
-            T = a.rag.len[t] + 1;
-            range_parts(T, P, kp);
-            F = range_fold_blocks(T, P, kp);
-        }
+        order_seq(a, t, st, T, P, kp, F);
         s_kp[t] = kp;
         s_P[t] = P;
         s_F[t] = F;
@@ -706,19 +786,7 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
         atomicAdd(&s_n[0], 1);
         atomicMax(&s_n[1], r0 + P);
         atomicMax(&s_n[2], fb0 + F);
-        RangeItem it{};
-        it.s = t;
-        it.P = P;
-        it.kp = kp;
-        it.len = T - 1;
-        it.next_pos = a.rag.next_pos[t];
-        it.base = a.rag.base[t];
-        for (int p = 0; p < P; ++p) {
-            it.p = p;
-            it.k0 = p * kp;
-            it.k1 = min(T, (p + 1) * kp);
-            rws.items[r0 + p] = it;
-        }
+        order_write(a, rws, t, T, P, kp, r0, fb0, false);  // fold entries below, spread over the block
     }
     __syncthreads();
     const int served = s_n[0], n_fold = s_n[2];
@@ -779,7 +847,8 @@ hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
 }  // namespace
 
 bool vz_decode_range_ok(int32_t L, int32_t Hkv, int32_t n_seqs) {
-    return static_cast<int64_t>(L) * Hkv >= RANGE_MIN_ITEMS && n_seqs <= RANGE_MAX_SEQS;
+    (void)n_seqs;  // any batch: the order kernel ranks up to RANGE_MAX_SEQS sequences, keeps the order beyond
+    return static_cast<int64_t>(L) * Hkv >= RANGE_MIN_ITEMS;
 }
 
 hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, bool fold, hipStream_t stream) {

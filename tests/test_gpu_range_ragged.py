@@ -1,7 +1,8 @@
 """GPU parity of the ragged decode call on the whole-range path (bf16, d = 128,
-at least 128 (layer, KV head) items, at most 1024 sequences): one order
-launch ranks the sequences' parts longest first, one workgroup per (part,
-layer, KV head), then the merge of sequences in parts and the fold.  Every
+at least 128 (layer, KV head) items): one order
+launch ranks the sequences' parts longest first (up to 1024 sequences; in
+sequence order beyond), one workgroup per (part, layer, KV head), then the
+merge of sequences in parts and the fold.  Every
 sequence is checked against the fp64 oracle on sampled layers and, bit for
 bit on every layer, against the single-sequence call on a copy of its data;
 slots outside every sequence stay untouched; the workspace starts filled
@@ -131,6 +132,17 @@ def test_ragged_range_many_sequences():
     lens = synth.uniform_int(key, 0, n, 0, 300).astype(np.int64)
     lens[:5] = [0, 127, 128, 1, 255]
     run_ragged(32, 4, 32, lens.tolist(), layers=[0, 31], seed=43, single_check=set(range(0, n, 10)))
+
+
+def test_ragged_range_more_sequences_than_one_order_block():
+    """1100 sequences of 0 to 40 keys (more than the 1024 the order kernel
+    ranks: sequence order, a block scan over runs of two sequences); layers
+    0 and 31; the single-call comparison on every fiftieth sequence."""
+    key = synth.stream_key(47, "more-seqs")
+    n = 1100
+    lens = synth.uniform_int(key, 0, n, 0, 40).astype(np.int64)
+    lens[:3] = [0, 40, 1]
+    run_ragged(32, 4, 32, lens.tolist(), layers=[0, 31], seed=47, gap=1, single_check=set(range(0, n, 50)))
 
 
 def test_ragged_range_gamma_edges():
