@@ -10,9 +10,10 @@ namespace {
 
 using namespace vz_mfma;
 
-// ---- whole-range path: single-sequence calls over many (layer, KV head) items ----
+// ---- whole-range path: calls over many (layer, KV head) items ----
 // One workgroup of RW waves per (layer, KV head) streams every key of the
-// head, so the softmax of its query heads completes inside the workgroup:
+// head (of a sequence, or of one part of it), so the softmax of its query
+// heads completes inside the workgroup:
 // wave w takes a contiguous run of about 1 / RW of the full 128-key chunks
 // (contiguous runs stream about 7 % faster than chunks dealt round-robin to
 // the waves), and wave 0 also the last, partial chunk: the first wave of each
@@ -26,9 +27,11 @@ using namespace vz_mfma;
 // the waves merge their (max, sum) pairs and outputs in LDS, the workgroup
 // writes its query heads' output rows, and every key's sum over those heads
 // of p_hj goes to the workspace.  A fold kernel then adds the KV heads' sums
-// into Eq. (6).  Compared with the chunked path there are no per-chunk
-// partial outputs or probabilities in HBM and no merge launch; it needs
-// enough (layer, KV head) items to occupy the GPU, one workgroup per CU.
+// into Eq. (6).  A part of a longer sequence instead leaves its statistics,
+// output and per-head probabilities relative to its own max, which a merge
+// kernel and the fold combine.  Compared with the chunked path there are no
+// per-chunk partial outputs or probabilities in HBM; it needs enough (layer,
+// KV head) items to occupy the GPU, one workgroup per CU.
 constexpr int RW = 8;                              // waves per workgroup (256 registers per lane)
 constexpr int RFULL = 8;                           // full chunks per wave
 constexpr int RNCH = RFULL + 1;                    // ... plus a last chunk of at most VT keys
@@ -213,7 +216,9 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     const int my_chunks = my_full + (w == 0 && part ? 1 : 0);
     // Chunk of the wave's slot k.  Wave 0 has the fewest full chunks
     // (n_full / RW), so the partial chunk is at most its slot RFULL, and there
-    // only when n_full = RW * RFULL, where the host limit leaves it <= VT keys.
+    // only when n_full = RW * RFULL, where the part limit (RANGE_MAX_KEYS keys
+    // for a whole sequence, RPART for a part of a longer one) leaves it <= VT
+    // keys.
     auto chunk_of = [&](int k) { return k < my_full ? c0 + k : n_full; };
     const size_t seq_row = static_cast<size_t>(it.s) * a.L + l;  // (sequence, layer) row of q, out, k_new, v_new
     const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base + it.k0) * D;
