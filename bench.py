@@ -76,6 +76,37 @@ def read_traffic():
     return float(m_b.group(1))
 
 
+def cpu_model() -> str:
+    """The host CPU's model string (Linux), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def copy_gbps(torch, stream, n_bytes: int = 1 << 30, reps: int = 10) -> float:
+    """Bytes moved (read + written) per second by a plain device-to-device
+    copy of n_bytes, timed with HIP events: the practical ceiling beside the
+    8 TB/s peak."""
+    a = torch.empty(n_bytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(2):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2 * n_bytes / (ms * 1e-3) / 1e9
+
+
 def cpu_baseline(w, n_layers_sample: int, max_seconds: float):
     """The oracle (as it stands) on a sample: the first n layers, fused on the
     host, then decode steps with eviction until max_seconds of step time."""
@@ -107,7 +138,7 @@ def cpu_baseline(w, n_layers_sample: int, max_seconds: float):
         "kind": "oracle",
         "sample": (f"{len(step_times)} decode steps (append, attend, score, evict) of the 32k workload on "
                    f"{n_layers_sample} of {w.n_layers} layers, after host-side fusion; time per step "
-                   f"scaled by {w.n_layers}/{n_layers_sample} to a whole-model token"),
+                   f"scaled by {w.n_layers}/{n_layers_sample} to a whole-model token; host CPU {cpu_model()}"),
     }
 
 
@@ -564,6 +595,7 @@ def main():
     step_bytes_ss = dec_bytes_ss + L * evict_bytes_per_layer(T_ss, 1, Hkv, d, s)
     traffic = read_traffic()
     fuse_bytes = L * Hkv * 2 * (32768 + n_spans) * d * s
+    copy_rate = copy_gbps(torch, stream)
 
     result = {
         "metric": "decode attend+score+evict tokens/s and HBM GB/s (% of peak) at 32k ctx",
@@ -608,6 +640,8 @@ def main():
             "algorithmic_bytes_per_launch": dec_bytes_ss,
             "mean_launch_us": dec_mean_s * 1e6,
             "launches_timed": args.roofline_calls,
+            "copy_gbps": copy_rate,
+            "frac_of_copy": achieved / copy_rate,
         },
     }
     if not args.no_cpu:
