@@ -225,3 +225,77 @@ def test_ragged_range_skips_invalid_and_overflowing_sequences():
     check_close(from_dev(Sd)[ls][:, :20001], ref_s, RTOL[DT], "score")
     assert np.array_equal(from_dev(Pd)[ls][:, :20001], ref_p)
     assert not from_dev(out_d)[1].any()
+
+
+def test_batch16_full_size_sampled_layers():
+    """The batched workload at full size, in the launch configuration bench.py
+    times: its 16 sequences' span counts (1,280 to 8,077 resident keys), 48
+    layers, 32Q/4KV, one ragged call per step on the whole-range path (3,072
+    range workgroups); two steps; every sequence against the oracle on layers
+    0, 23 and 47, three sequences bit for bit on every layer against their
+    single calls.  The device state is written sequence by sequence, so the
+    host holds one sequence's layers at a time."""
+    t = torch()
+    import paper_2608_08569_amd as vz
+    ws_list = synth.batch_workloads()
+    w0 = ws_list[0]
+    L, Hq, Hkv = w0.n_layers, w0.n_q_heads, w0.kv_heads
+    n = len(ws_list)
+    lens = np.array([len(synth.offsets_from_lengths(synth.span_lengths(w, seq=i))) - 1
+                     for i, w in enumerate(ws_list)], dtype=np.int64)
+    caps = np.maximum(lens, [w.budget for w in ws_list]) + w0.interval + 1
+    next_pos = lens.copy()
+    pk = Packed(caps, gap=0, seed=0)
+    Kd = t.empty(L, Hkv, pk.total, D, dtype=t.bfloat16, device="cuda")
+    Vd = t.empty_like(Kd)
+    Sd = t.empty(L, pk.total, dtype=t.float32, device="cuda")
+    Pd = t.empty(L, pk.total, dtype=t.int32, device="cuda")
+    for s in range(n):
+        k, v, sc, p = layered_state(60 + s, L, Hkv, D, int(caps[s]), int(lens[s]), DT, int(next_pos[s]))
+        sl = pk.sl(s)
+        Kd[:, :, sl].copy_(to_dev(k))
+        Vd[:, :, sl].copy_(to_dev(v))
+        Sd[:, sl].copy_(t.from_numpy(sc))
+        Pd[:, sl].copy_(t.from_numpy(p))
+        del k, v
+    base_d, cap_d = pk.dev()
+    len_d, next_d = _i32(lens), _i32(next_pos)
+    status = _i32(np.full(n, -99))
+    out_d = t.zeros(n, L, Hq, D, dtype=t.bfloat16, device="cuda")
+    ws = vz.workspace_ragged(vz.VZ_OP_DECODE, L, Hq, Hkv, D, pk.total, n)
+    ls = [0, 23, 47]
+    whole = [2, 9, 15]  # shortest, a middle one, longest
+    for step in range(2):
+        q, kn, vn = _inputs(61, step, n, L, Hq, Hkv)
+        t.cuda.synchronize()
+        K0, V0 = from_dev(Kd[ls]), from_dev(Vd[ls])
+        S0, P0 = from_dev(Sd), from_dev(Pd)
+        before = {s: (from_dev(Kd[:, :, pk.sl(s)]), from_dev(Vd[:, :, pk.sl(s)])) for s in whole}
+        vz.voxzip_decode_attend_score_ragged(to_dev(q), to_dev(kn), to_dev(vn), Kd, Vd, Sd, Pd, out_d, base_d,
+                                             cap_d, len_d, next_d, w0.gamma, status=status, workspace=ws)
+        t.cuda.synchronize()
+        assert np.all(from_dev(status) == vz.VZ_OK)
+        out, S1, P1 = from_dev(out_d), from_dev(Sd), from_dev(Pd)
+        for s in range(n):
+            sl, ln, npos = pk.sl(s), int(lens[s]), int(next_pos[s])
+            ref_o, ref_s, ref_p, _ = oracle.decode_step(q[s][ls], kn[s][ls], vn[s][ls], K0[:, :, sl], V0[:, :, sl],
+                                                        S0[ls][:, sl].astype(np.float64), P0[ls][:, sl], ln, npos,
+                                                        w0.gamma, DT)
+            check_close(widen(out[s][ls], DT), ref_o, RTOL[DT], f"step {step} seq {s} output")
+            check_close(S1[ls][:, sl][:, : ln + 1], ref_s, RTOL[DT], f"step {step} seq {s} score")
+            assert np.array_equal(P1[ls][:, sl][:, : ln + 1], ref_p)
+        for s in whole:
+            sl, ln, npos = pk.sl(s), int(lens[s]), int(next_pos[s])
+            g = GpuCache(L, Hq, Hkv, D, int(caps[s]), DT)
+            g.load(before[s][0], before[s][1], S0[:, sl], P0[:, sl], ln, npos)
+            g.step(to_dev(q[s]), to_dev(kn[s]), to_dev(vn[s]), w0.gamma)
+            Kg, Vg, Sg, Pg = g.snapshot()
+            assert np.array_equal(from_dev(g.out), out[s]), f"step {step} seq {s}: output differs from the single call"
+            assert np.array_equal(Sg, S1[:, sl]) and np.array_equal(Pg, P1[:, sl])
+            assert np.array_equal(Kg, from_dev(Kd[:, :, sl])) and np.array_equal(Vg, from_dev(Vd[:, :, sl]))
+            del g, Kg, Vg
+        del before, K0, V0
+        len_d += 1
+        next_d += 1
+        lens += 1
+        next_pos += 1
