@@ -27,6 +27,7 @@ def _state(L, Hq, Hkv, d, cap, length, dtype, seed):
 
 @pytest.mark.parametrize("Hq,Hkv,L,length,budget,dtype,d,kept", [
     (32, 4, 32, 8192, 8192, synth.DT_BF16, 128, False),    # fused, E = 1
+    (32, 4, 48, 8192, 8192, synth.DT_BF16, 128, False),    # fused, E = 1: the shape bench.py times
     (32, 4, 32, 8192, 8190, synth.DT_BF16, 128, True),     # fused, E = 3, kept positions
     (32, 4, 32, 8192, 8000, synth.DT_BF16, 128, False),    # fused, E = 193: radix select
     (32, 4, 32, 6000, 9000, synth.DT_BF16, 128, True),     # fused, no eviction, kept positions only
