@@ -107,6 +107,80 @@ def copy_gbps(torch, stream, n_bytes: int = 1 << 30, reps: int = 10) -> float:
     return 2 * n_bytes / (ms * 1e-3) / 1e9
 
 
+def cpu_report(max_seconds: float = 8.0) -> dict:
+    """The oracle as it stands, timed on the host per workload: single-threaded
+    and with its OpenMP loop over layers on several cores (the batch: a pool
+    of threads over sequences, one oracle thread each).  The layer workload
+    runs whole; long32k and aggr64k on a sample of layers and batch16 on
+    layer 0 of every sequence, their step times scaled to whole-model
+    tokens.  Each run steps until max_seconds; the first step of aggr64k
+    holds its large eviction.  Reports median step times and tokens/s."""
+    import concurrent.futures as cf
+    import oracle
+    lib = oracle.load()
+    n_all = oracle.threads(lib)
+    rep = {"cpu_model": cpu_model(), "nproc": os.cpu_count(), "omp_max_threads": n_all, "workloads": []}
+
+    def timed(step, steps_max):
+        times, t_all = [], time.time()
+        for t in range(steps_max):
+            ts = time.perf_counter()
+            step(t)
+            times.append(time.perf_counter() - ts)
+            if time.time() - t_all > max_seconds:
+                break
+        return float(np.median(times)), len(times)
+
+    for name in ("layer", "long32k", "aggr64k"):
+        w = synth.workload(name)
+        off = synth.offsets_from_lengths(synth.span_lengths(w))
+        n = len(off) - 1
+        for threads in ((1,) if w.n_layers == 1 else (1, min(n_all, 8))):
+            sample = 1 if w.n_layers == 1 else (2 if threads == 1 else threads)
+            ls = range(min(sample, w.n_layers))
+            oracle.set_threads(threads, lib)
+            run = oracle.Run(synth.prefill_kv(w, "k", layers=ls), synth.prefill_kv(w, "v", layers=ls), off, w.dtype,
+                             w.n_q_heads, max(n, w.budget) + 4, w.gamma, w.budget, lib=lib)
+            ins = [synth.decode_inputs(w, t) for t in range(8)]
+
+            def step(t, run=run, ins=ins, k=len(ls)):
+                q, kn, vn = ins[t % len(ins)]
+                run.step(q[:k], kn[:k], vn[:k])
+            med, steps = timed(step, w.steps)
+            per_token = med * w.n_layers / len(ls)
+            rep["workloads"].append({"workload": name, "threads": min(threads, len(ls)), "layers_sampled": len(ls),
+                                     "steps_timed": steps, "ms_per_token": per_token * 1e3,
+                                     "tokens_per_s": 1.0 / per_token})
+            log(f"[cpu] {name}, {threads} thread(s): {per_token * 1e3:.1f} ms per token")
+    ws_list = synth.batch_workloads()
+    runs = []
+    oracle.set_threads(1, lib)
+    for i, w in enumerate(ws_list):
+        off = synth.offsets_from_lengths(synth.span_lengths(w, seq=i))
+        n = len(off) - 1
+        runs.append(oracle.Run(synth.prefill_kv(w, "k", seq=i, layers=range(1)),
+                               synth.prefill_kv(w, "v", seq=i, layers=range(1)), off, w.dtype, w.n_q_heads,
+                               max(n, w.budget) + w.interval + 1, w.gamma, w.budget, interval=w.interval, lib=lib))
+    w0 = ws_list[0]
+    b_ins = [[tuple(x[:1] for x in synth.decode_inputs(w, t, seq=i)) for t in range(4)] for i, w in enumerate(ws_list)]
+    for threads in (1, min(n_all, len(runs))):
+        pool = cf.ThreadPoolExecutor(threads)
+
+        def one(i, t):
+            runs[i].step(*b_ins[i][t % 4])
+
+        def step(t):
+            list(pool.map(lambda i: one(i, t), range(len(runs))))
+        med, steps = timed(step, w0.steps)
+        pool.shutdown()
+        per_step = med * w0.n_layers  # all 16 sequences, 48 layers: 16 tokens
+        rep["workloads"].append({"workload": "batch16", "threads": threads, "layers_sampled": 1, "steps_timed": steps,
+                                 "ms_per_token": per_step / len(runs) * 1e3, "tokens_per_s": len(runs) / per_step})
+        log(f"[cpu] batch16, {threads} thread(s): {per_step / len(runs) * 1e3:.1f} ms per token")
+    oracle.set_threads(n_all, lib)
+    return rep
+
+
 def cpu_baseline(w, n_layers_sample: int, max_seconds: float):
     """The oracle (as it stands) on a sample: the first n layers, fused on the
     host, then decode steps with eviction until max_seconds of step time."""
@@ -457,6 +531,8 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-report", action="store_true",
+                    help="only time the CPU oracle per workload (single- and multi-threaded); no GPU work")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--workload", default="long32k",
@@ -470,6 +546,10 @@ def main():
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(the sharding design is described in the design notes)", file=sys.stderr)
         sys.exit(2)
+
+    if args.cpu_report:
+        print(json.dumps(cpu_report()), flush=True)
+        return
 
     import torch
     import paper_2608_08569_amd as vz

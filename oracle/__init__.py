@@ -44,6 +44,8 @@ def load(path: str | None = None):
     P = ctypes.c_void_p
     i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
     lib.orc_threads.restype = ctypes.c_int
+    lib.orc_set_threads.argtypes = [ctypes.c_int]
+    lib.orc_set_threads.restype = None
     lib.orc_fuse.argtypes = [P, i32, P, i32, P, i32, i32, i32, i32, P]
     lib.orc_decode_step.argtypes = [P, P, P, P, P, P, P, i32, i32, f64, f64,
                                     i32, i32, i32, i32, i32, i32, P, P, P, P]
@@ -70,6 +72,11 @@ def _store(a, dtype):
 
 def threads(lib=None) -> int:
     return (lib or load()).orc_threads()
+
+
+def set_threads(n: int, lib=None) -> None:
+    """Threads of the oracle's parallel loops from now on (timing only)."""
+    (lib or load()).orc_set_threads(int(n))
 
 
 def fuse(x, off, dtype, anchor=None, lib=None):

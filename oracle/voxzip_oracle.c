@@ -62,6 +62,17 @@ int orc_threads(void)
 #endif
 }
 
+/* Threads of the later parallel loops (timing only; the results do not
+ * depend on it: every loop iteration is one layer, summed in its own order). */
+void orc_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Eq. (4): out[l][h][j][:] = (1/|G_j|) * sum_{k in G_j} x[l][h][k][:], where
  * G_j = [off[j], off[j+1]); then + anchor[l][h][j][:] when an anchor is given. */
 int orc_fuse(const void *x, int32_t T_in, const int32_t *off, int32_t n_spans,
