@@ -78,3 +78,30 @@ def test_deterministic_bits():
     b = _check_evict(2, 4, 128, 1800, 1500, 1000, synth.DT_BF16, next_pos=1600, seed=9).snapshot()
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+def test_worked_selection_from_the_golden_file():
+    """The library's eviction on the hand-worked case of
+    tests/golden/stage2_select_worked.json (fp32 cache, d = 64, one layer):
+    the kept positions and the rows that stay, keyed by position."""
+    import json
+    import os
+    import torch
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "stage2_select_worked.json")))
+    x = g["input"]
+    n, B = len(x["positions"]), x["budget"]
+    k = (np.arange(n * 64, dtype=np.float32).reshape(1, 1, n, 64) + 1.0)
+    v = -k
+    s = np.array([x["scores"]], dtype=np.float32)
+    p = np.array([x["positions"]], dtype=np.int32)
+    gc = GpuCache(1, 8, 1, 64, n, synth.DT_F32)
+    gc.load(k, v, s, p, n, x["next_pos"])
+    kept = torch.full((1, B), -1, dtype=torch.int32, device="cuda")
+    assert gc.evict(B, kept=kept) == B
+    assert from_dev(kept)[0].tolist() == g["kept_positions"]
+    K, V, S, P = gc.snapshot()
+    order = np.argsort(P[0, :B], kind="stable")
+    assert P[0, :B][order].tolist() == g["kept_positions"]
+    want = np.array(g["kept_positions"])
+    assert np.array_equal(K[0, 0, :B][order], k[0, 0, want]) and np.array_equal(V[0, 0, :B][order], v[0, 0, want])
+    assert np.array_equal(S[0, :B][order], s[0, want])

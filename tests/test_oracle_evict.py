@@ -89,3 +89,21 @@ def test_rejects_windows_larger_than_budget():
     _, _, score, pos = synth.random_state(4, 1, 1, 4, 64, 50, 0, next_pos=50)
     with pytest.raises(ValueError):
         oracle.evict_select(score, pos, 50, 20, 4, 17, 50)
+
+
+def _golden_select():
+    import json
+    import os
+    return json.load(open(os.path.join(os.path.dirname(__file__), "golden", "stage2_select_worked.json")))
+
+
+def test_worked_selection_from_the_golden_file():
+    """The kept set worked out by hand in tests/golden/stage2_select_worked.json
+    (three scores tie for the last two places: the smaller positions win)."""
+    g = _golden_select()
+    x = g["input"]
+    score = np.array([x["scores"]], dtype=np.float32).astype(np.float64)
+    pos = np.array([x["positions"]], dtype=np.int32)
+    keep, nl = oracle.evict_select(score, pos, len(x["positions"]), x["budget"], 4, -1, x["next_pos"])
+    assert nl == x["budget"]
+    assert pos[0][keep[0]].tolist() == g["kept_positions"]

@@ -71,3 +71,17 @@ def test_worked_cases():
 def test_invalid_arguments_are_rejected(args):
     with pytest.raises(vz.VoxzipError):
         vz.voxzip_build_span_offsets([0], [10], np.array([0.9], np.float32), [1], **args)
+
+
+def test_worked_example_from_the_golden_file():
+    """A segment list worked out by hand (tests/golden/stage1_offsets_worked.json:
+    a dropped low-confidence segment, an overlap clipped to the previous end,
+    more text tokens than audio tokens, background tokens): the oracle and
+    the library give the hand-derived offsets."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "stage1_offsets_worked.json")))
+    x = g["input"]
+    got = _both(np.array(x["t_start_ms"]), np.array(x["t_end_ms"]), np.array(x["conf"], dtype=np.float32),
+                np.array(x["text_len"]), x["t_total_ms"], x["L_a"])
+    assert got.tolist() == g["offsets"]
