@@ -47,7 +47,9 @@ inline __host__ __device__ int64_t range_row(int64_t plane) { return (plane + CH
 
 // Parts of a sequence of T keys: one part when T <= RANGE_MAX_KEYS, else the
 // fewest parts of kp keys (a multiple of RFOLD_KEYS, at most RPART), the last
-// part holding the remaining T - (P - 1) kp >= 1 keys.
+// part holding the remaining T - (P - 1) kp >= 1 keys.  (Rounding P up so
+// that the workgroups fill whole rounds of the CUs measured no faster: 2 or 4
+// parts of a 12k- or 16k-key cache took the same time.)
 __host__ __device__ inline void range_parts(int T, int& P, int& kp) {
     if (T <= RANGE_MAX_KEYS) {
         P = 1;
@@ -177,11 +179,14 @@ __device__ __forceinline__ RangeItem uniform_item(const RangeItem& x) {
     return it;
 }
 
-// Grid (Hkv, L, parts): workgroup (g, l, r) takes KV head g of layer l over
-// the keys of item r.  RAG: items from the ragged call's table (dispatch
-// order longest first); else the parts of the single sequence.  SPLIT: items
-// may be parts of a longer sequence, whose statistics, outputs and per-head
-// probabilities go to the workspace for the merge and fold kernels.
+// Grid (NW, L) for a sequence of one part; NW x L x items, flattened, for
+// parts and ragged calls (KV head fastest, then layer, then item, so a
+// ragged call's items go out in the table's order): workgroup (g, l, r)
+// takes KV head g of layer l over the keys of item r.  RAG: items from the
+// ragged call's table (dispatch order longest first); else the parts of the
+// single sequence.  SPLIT: items may be parts of a longer sequence, whose
+// statistics, outputs and per-head probabilities go to the workspace for the
+// merge and fold kernels.
 template <int NW, bool RAG, bool SPLIT>
 __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArgs a) {
     static_assert(RW * GMAX * RO_STRIDE * 4 <= RW * TILE_BYTES, "the merged outputs fit in the tile buffers");
@@ -197,7 +202,10 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     const int q4 = lane >> 4, r16 = lane & 15;
     const int hi = r16 >> 3, hh = r16 & 7;
     const int Hq = a.Hq, G = Hq / NW;
-    const int g = blockIdx.x, l = blockIdx.y, r = blockIdx.z;
+    constexpr bool FLAT = RAG || SPLIT;
+    const int g = FLAT ? static_cast<int>(blockIdx.x) % NW : static_cast<int>(blockIdx.x);
+    const int l = FLAT ? (static_cast<int>(blockIdx.x) / NW) % a.L : static_cast<int>(blockIdx.y);
+    const int r = FLAT ? static_cast<int>(blockIdx.x) / (NW * a.L) : 0;
     const RangeWs rws = range_ws<NW>(a, RAG);
     RangeItem it;
     if constexpr (RAG) {
@@ -828,20 +836,21 @@ template <int NW>
 hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
     if (a.rag.n > 0) {
         hipLaunchKernelGGL((range_order_kernel<NW>), dim3(1), dim3(ORDER_THREADS), 0, stream, a);
-        hipLaunchKernelGGL((decode_range_kernel<NW, true, true>), dim3(NW, a.L, a.R), dim3(64 * RW), 0, stream, a);
+        hipLaunchKernelGGL((decode_range_kernel<NW, true, true>), dim3(NW * a.L * a.R), dim3(64 * RW), 0, stream, a);
         hipLaunchKernelGGL((range_merge_kernel<NW, true>), dim3(a.R, a.L), dim3(RMERGE_THREADS), 0, stream, a);
         hipLaunchKernelGGL((range_fold_parts_kernel<NW, true>), dim3(a.FB, a.L), dim3(RFOLD_KEYS), 0, stream, a);
         return hipGetLastError();
     }
     if (a.n_parts > 1) {
-        hipLaunchKernelGGL((decode_range_kernel<NW, false, true>), dim3(NW, a.L, a.n_parts), dim3(64 * RW), 0, stream, a);
+        hipLaunchKernelGGL((decode_range_kernel<NW, false, true>), dim3(NW * a.L * a.n_parts), dim3(64 * RW), 0,
+                           stream, a);
         hipLaunchKernelGGL((range_merge_kernel<NW, false>), dim3(1, a.L), dim3(RMERGE_THREADS), 0, stream, a);
         hipLaunchKernelGGL((range_fold_parts_kernel<NW, false>),
                            dim3(range_fold_blocks(a.len + 1, a.n_parts, a.part_keys), a.L), dim3(RFOLD_KEYS), 0,
                            stream, a);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((decode_range_kernel<NW, false, false>), dim3(NW, a.L, 1), dim3(64 * RW), 0, stream, a);
+    hipLaunchKernelGGL((decode_range_kernel<NW, false, false>), dim3(NW, a.L), dim3(64 * RW), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !fold) return e;
     hipLaunchKernelGGL((decode_range_fold_kernel<NW>), dim3((a.len + RFOLD_THREADS) / RFOLD_THREADS, a.L),
@@ -865,7 +874,6 @@ hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, bool fold, h
         range_parts(a.len + 1, a.n_parts, a.part_keys);
         a.R = a.n_parts;
         a.FB = 0;
-        if (a.n_parts > 65535) return hipErrorInvalidValue;  // grid z
     }
     switch (Hkv) {
         case 1: return launch_range<1>(a, fold, stream);
