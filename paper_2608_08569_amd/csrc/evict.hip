@@ -129,11 +129,17 @@ struct SelJob {
     int32_t* kept;
     int32_t len, budget, n_sink, M, next_pos, Hkv;
     int inline_kv;
+    // READY callers: this thread's smallest competing key and its slot
+    // (~0 and -1 without one), which the first minimum round uses instead of
+    // reading the keys back
+    uint64_t first_best;
+    int32_t first_best_j;
 };
 
 // LK: this layer's keys are kept in LDS (needs sh.keys and len <= kLdsSlots
 // and inline_kv).  READY: the caller has already filled sh.keys (and passed a
-// barrier); only with LK.
+// barrier) and passes each thread's smallest key; only with LK.  With one
+// eviction the keys are never read back, so such a caller may leave them out.
 // move_fn(n_moves, src, dst), when given, may perform the moves itself (and
 // return true) instead of the copies below.
 template <int DT, int D, bool LK, class SH, bool READY = false, class MoveFn = std::nullptr_t>
@@ -205,12 +211,17 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh,
         for (int r = 0; r < E; ++r) {
             uint64_t best = ~0ull;
             int best_j = -1;
-            for (int j = tid; j < len; j += kSel) {
-                uint64_t k;
-                if (!key_at(j, k)) continue;
-                if (k > tau && k < best) {
-                    best = k;
-                    best_j = j;
+            if (READY && r == 0) {
+                best = job.first_best;
+                best_j = job.first_best_j;
+            } else {
+                for (int j = tid; j < len; j += kSel) {
+                    uint64_t k;
+                    if (!key_at(j, k)) continue;
+                    if (k > tau && k < best) {
+                        best = k;
+                        best_j = j;
+                    }
                 }
             }
             tau = block_min_u64(best, sh);
@@ -476,6 +487,11 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
         piece_base = (which ? v0 : k0) + h * head_stride + c * PER;
         piece = *reinterpret_cast<const uint4*>(piece_base + static_cast<size_t>(piece_slot) * D);
     }
+    // the keys go to LDS only for the later minimum rounds (E >= 2) and the
+    // radix select; the first round takes each thread's smallest key
+    const bool keys_to_lds = E >= 2;
+    uint64_t my_best = ~0ull;
+    int my_best_j = -1;
     auto fold_keys = [&](auto per_thread) {
         constexpr int B = decltype(per_thread)::value;
         int32_t pv[B];
@@ -498,7 +514,12 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
                 const float a_new = fmaf(f.gamma, j < len - 1 ? av[b] : 0.f, acc);
                 A[j] = a_new;
                 const int32_t p = pv[b];
-                sh.keys[j] = p >= a.n_sink && p < recent_from ? vz::rank_key(a_new, p) : kNoKey;
+                const uint64_t key = p >= a.n_sink && p < recent_from ? vz::rank_key(a_new, p) : kNoKey;
+                if (keys_to_lds) sh.keys[j] = key;
+                if (key < my_best) {  // kNoKey never wins: keys hold the position, so they are below ~0
+                    my_best = key;
+                    my_best_j = j;
+                }
                 if (pre && j >= a.budget) {
                     sh.pre_a[j - a.budget] = a_new;
                     sh.pre_p[j - a.budget] = p;
@@ -530,6 +551,8 @@ __global__ __launch_bounds__(kSel) void fold_select_kernel(const VzEvictArgs a, 
     job.next_pos = a.next_pos;
     job.Hkv = a.Hkv;
     job.inline_kv = 1;
+    job.first_best = my_best;
+    job.first_best_j = my_best_j;
     // the moves from the prefetched rows (pairs in LDS, at most kSmallE)
     auto move_pre = [&](int n_moves, const int32_t* src, const int32_t* dst) -> bool {
         if (!pre) return false;
