@@ -227,12 +227,24 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh,
             tau = block_min_u64(best, sh);
             if (tau == ~0ull) break;  // fewer middle slots than E
             // keys are distinct (they hold the position), so one thread owns the minimum
-            if (LK && best == tau) s_ev[r] = best_j;
+            if (LK && best == tau) {
+                s_ev[r] = best_j;
+                if (E == 1) {
+                    // one eviction: len = budget + 1, so slot `budget` is the only
+                    // slot at or past the budget, and it moves into the hole
+                    // unless it is the evicted one
+                    sh.nm = best_j < budget ? 1 : 0;
+                    s_src[0] = budget;
+                    s_dst[0] = best_j;
+                }
+            }
             ++found;
         }
         thr = tau;
         shift = 0;
-        if (LK) {
+        if (LK && E == 1 && found == 1) {
+            __syncthreads();  // the pair the minimum's owner wrote
+        } else if (LK) {
             // Holes: evicted slots below the budget; movers: kept slots at or
             // above it; the k-th mover fills the k-th hole, both in slot order
             // (at most kSmallE of each, so one thread pairs them).
