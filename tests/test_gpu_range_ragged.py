@@ -299,3 +299,51 @@ def test_batch16_full_size_sampled_layers():
         next_d += 1
         lens += 1
         next_pos += 1
+
+
+def test_ragged_range_calls_on_two_streams():
+    """Two packed batches decoded at the same time on two streams, each with
+    its own workspace, give the bits of the same calls run one after the
+    other: the path keeps all of its state in the workspace, and no
+    workgroup waits for another."""
+    t = torch()
+    import paper_2608_08569_amd as vz
+    L, Hq, Hkv = 32, 32, 4
+    batches = []
+    for seed, lens in ((71, [300, 5000, 9000, 17]), (72, [8000, 64, 2500])):
+        lens = np.asarray(lens, dtype=np.int64)
+        n = len(lens)
+        next_pos = lens + 5
+        caps = lens + 3
+        pk = Packed(caps, gap=2, seed=seed)
+        K, V, S, P = _packed(pk, L, Hkv, lens, next_pos, seed)
+        q, kn, vn = _inputs(seed, 0, n, L, Hq, Hkv)
+        batches.append(dict(pk=pk, state=(K, V, S, P), ins=(q, kn, vn), lens=lens, next_pos=next_pos, n=n))
+
+    def run(streams):
+        outs = []
+        for b, st in zip(batches, streams):
+            K, V, S, P = b["state"]
+            d = dict(K=to_dev(K), V=to_dev(V), S=to_dev(S), P=to_dev(P),
+                     out=t.zeros(b["n"], L, Hq, D, dtype=t.bfloat16, device="cuda"),
+                     ws=vz.workspace_ragged(vz.VZ_OP_DECODE, L, Hq, Hkv, D, b["pk"].total, b["n"]),
+                     ins=[to_dev(x) for x in b["ins"]], base_cap=b["pk"].dev(), len=_i32(b["lens"]),
+                     nxt=_i32(b["next_pos"]))
+            outs.append(d)
+        t.cuda.synchronize()
+        for d, st in zip(outs, streams):
+            with t.cuda.stream(st):
+                vz.voxzip_decode_attend_score_ragged(*d["ins"], d["K"], d["V"], d["S"], d["P"], d["out"],
+                                                     d["base_cap"][0], d["base_cap"][1], d["len"], d["nxt"], 0.95,
+                                                     workspace=d["ws"], stream=st)
+            if len(set(streams)) == 1:
+                t.cuda.synchronize()
+        t.cuda.synchronize()
+        return [tuple(from_dev(d[k]) for k in ("out", "K", "V", "S", "P")) for d in outs]
+
+    s0 = t.cuda.current_stream()
+    seq = run([s0, s0])
+    par = run([t.cuda.Stream(), t.cuda.Stream()])
+    for a, b in zip(seq, par):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
