@@ -97,19 +97,14 @@ __device__ __forceinline__ float wave_sum(float v) {
     for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
     return v;
 }
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
-    uint32_t lo = static_cast<uint32_t>(v), hi = static_cast<uint32_t>(v >> 32);
-    lo = __shfl_xor(lo, o, kWave);
-    hi = __shfl_xor(hi, o, kWave);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
-}
+// Minimum over the wave (every lane active): the high words first, then the
+// low words of the lanes holding that high word; two cross-lane (DPP)
+// reductions instead of six dependent 64-bit shuffles through LDS.
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        uint64_t w = shfl_xor_u64(v, o);
-        v = w < v ? w : v;
-    }
-    return v;
+    const uint32_t hi = static_cast<uint32_t>(v >> 32), lo = static_cast<uint32_t>(v);
+    const uint32_t hmin = __reduce_min_sync(~0ull, hi);
+    const uint32_t lmin = __reduce_min_sync(~0ull, hi == hmin ? lo : 0xFFFFFFFFu);
+    return (static_cast<uint64_t>(hmin) << 32) | lmin;
 }
 __device__ __forceinline__ int wave_sum_i(int v) {
 #pragma unroll
