@@ -22,7 +22,7 @@
 //           registers (DPP row rotate by 8), so 128 keys x 8 heads take 16
 //           registers per lane.
 //   stats   chunk-local max m_c and sum l_c of exp2 per head; the registers
-//           then hold p~ = exp2(s - m_c).  (m_c, l_c) and p~ (half precision,
+//           then hold p~ = exp2(s - m_c).  (m_c, l_c) and p~ (bfloat16,
 //           64 bytes per key over the 32 heads of the workload) go to the
 //           workspace.
 //   pass 2  O_c = P V: V tiles take the same coalesced path into LDS and are
@@ -48,7 +48,7 @@ constexpr size_t kHeaderBytes = 256;  // decode workspace header (unused by this
 // Per-chunk partial results in the workspace, after the header:
 //   ml [L][nc_max][Hq]        float2     chunk max m_c and sum l_c of exp2, per head
 //   o  [L][nc_max][Hq][D]     bfloat16   O_c relative to m_c
-//   p  [L][nc_max][Hq][CHUNK] half       p~ = exp2(s - m_c) per key of the chunk
+//   p  [L][nc_max][Hq][CHUNK] bfloat16   p~ = exp2(s - m_c) per key of the chunk
 //   layer [S][L][Hq]          float2     the layer's max M and 1 / sum S, per head
 //                                        (S = sequences of the call)
 template <typename B>
@@ -320,7 +320,7 @@ __global__ __launch_bounds__(64 * NW, DEPTH == 1 ? ATTEND_WG_PER_CU : 1) void de
         __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
     // ---------------- partial results: whole rows through LDS ----------------
-    // p~ (half, CHUNK entries per head) and O (bfloat16 relative to the chunk
+    // p~ (bfloat16, CHUNK entries per head) and O (bfloat16 relative to the chunk
     // max, 256 bytes per head) of the wave's G heads are staged in its free
     // tile buffer at padded per-head strides, then written as 1 KB fully
     // coalesced stores: the workspace holds both as rows, heads of the wave
@@ -334,7 +334,7 @@ __global__ __launch_bounds__(64 * NW, DEPTH == 1 ? ATTEND_WG_PER_CU : 1) void de
 #pragma unroll
             for (int u = 0; u < PAIRS; ++u)
                 *reinterpret_cast<uint2*>(lp + hh * HSP + 2 * (VT * u + 16 * hi + 4 * q4)) =
-                    make_uint2(pack_f16x2(sp[u][0], sp[u][1]), pack_f16x2(sp[u][2], sp[u][3]));
+                    make_uint2(pack_bf16x2(sp[u][0], sp[u][1]), pack_bf16x2(sp[u][2], sp[u][3]));
         }
         if (r16 < G) {
 #pragma unroll
@@ -517,7 +517,7 @@ __global__ __launch_bounds__(CHUNK) void decode_fold_kernel(const FusedArgs a) {
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < FOLD_HEADS; ++q)
-            if (hb + q < Hq) acc = fmaf(f16_to_f32(pr[q]), s_f[q], acc);
+            if (hb + q < Hq) acc = fmaf(vz::bf16_to_f32(pr[q]), s_f[q], acc);
         __syncthreads();
     }
     if (t < nk) *sc = fmaf(a.gamma, a_old, acc);
@@ -621,7 +621,7 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < FOLD_HEADS; ++q)
-            if (hb + q < Hq) acc = fmaf(f16_to_f32(pr[q]), s_f[q], acc);
+            if (hb + q < Hq) acc = fmaf(vz::bf16_to_f32(pr[q]), s_f[q], acc);
         __syncthreads();
     }
     if (t < CHUNK && t < nk) *sc = fmaf(a.gamma, a_old, acc);

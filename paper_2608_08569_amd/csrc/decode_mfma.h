@@ -50,23 +50,22 @@ __device__ __forceinline__ float ror8(float v) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kRor8, 0xF, 0xF, false));
 }
 
+// Two floats to packed bfloat16 (low half a), round to nearest even: one
+// v_cvt_pk_bf16_f32 on gfx950 (the same bits as vz::f32_to_bf16 for finite
+// values).  Used for the P operand of the P.V products and for the stored
+// probabilities p~, which keep 8 significant bits at any magnitude (no
+// subnormal range to fall into, unlike half precision).
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    return static_cast<uint32_t>(vz::f32_to_bf16(a)) | (static_cast<uint32_t>(vz::f32_to_bf16(b)) << 16);
+    const bf16x2_t r = __builtin_convertvector(f32x2_t{a, b}, bf16x2_t);
+    uint32_t u;
+    __builtin_memcpy(&u, &r, 4);
+    return u;
 }
-
-// Half precision (round to nearest even) pack / unpack.
-__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-    const _Float16 ha = static_cast<_Float16>(a), hb = static_cast<_Float16>(b);
-    uint16_t ua, ub;
-    __builtin_memcpy(&ua, &ha, 2);
-    __builtin_memcpy(&ub, &hb, 2);
-    return static_cast<uint32_t>(ua) | (static_cast<uint32_t>(ub) << 16);
-}
-__device__ __forceinline__ float f16_to_f32(uint16_t x) {
-    _Float16 h;
-    __builtin_memcpy(&h, &x, 2);
-    return static_cast<float>(h);
-}
+// The low and high bfloat16 of a packed pair, widened.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Kernel arguments shared by the decode launches.  A single-sequence call
 // has rag.n == 0 and takes len, next_pos and n_chunks from here; a ragged

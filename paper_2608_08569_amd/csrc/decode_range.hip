@@ -21,7 +21,7 @@ using namespace vz_mfma;
 // the second, so work added to it stays off the critical path.  Each wave
 // keeps, per head, a running
 // max, sum and output (online softmax, the output rescaled whenever the max
-// grows), plus each chunk's p~ = exp2(s - m_ref) in half precision (the
+// grows), plus each chunk's p~ = exp2(s - m_ref) in bfloat16 (the
 // first RLDS chunks in LDS, the others in registers) and the reference max
 // m_ref it was taken against.  At the end
 // the waves merge their (max, sum) pairs and outputs in LDS, the workgroup
@@ -79,7 +79,7 @@ static_assert(sizeof(RangeItem) == 64, "one 64-byte record per item");
 //   sums  [L][Hkv][row] float          per key, the sum over the KV head's query
 //                                      heads of p_hj (sequences of one part;
 //                                      rows padded to whole chunks)
-//   rows  [L][Hkv][row][GMAX] half     per key and query head, p_hj relative to
+//   rows  [L][Hkv][row][GMAX] bf16     per key and query head, p_hj relative to
 //                                      its part's max (sequences of several parts)
 //   pstat [L][Hkv][R][GMAX] float2     each part's max and sum of exp2, per head
 //   pout  [L][Hkv][R][GMAX][D] float   each part's output relative to its max
@@ -156,7 +156,7 @@ __device__ __forceinline__ RangeItem single_item(const FusedArgs& a, int r) {
     return it;
 }
 
-// Row of key r (0..CHUNK-1) in a chunk's [key][head] half-precision rows
+// Row of key r (0..CHUNK-1) in a chunk's [key][head] bfloat16 rows
 // (16 bytes each): bit 1 is flipped by bit 4, so that the 8 keys one write
 // instruction covers (r = c + 4 q4 + 16 hi) start on 8 distinct 4-bank groups.
 __device__ __forceinline__ int pslot(int r) { return r ^ ((r >> 3) & 2); }
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[RW][TILE_BYTES];
     __shared__ float2 s_stat[RW][GMAX];
     // p~ of the first RLDS chunks of each wave, transposed: [slot(key)][head]
-    // in half precision (16 bytes per key; slot() in the head-sum epilogue)
+    // in bfloat16 (16 bytes per key; slot() in the head-sum epilogue)
     __shared__ __attribute__((aligned(16))) uint16_t s_pt[RW][RLDS][CHUNK][GMAX];
     __shared__ __attribute__((aligned(16))) float s_mref[RW][RNCH][GMAX];  // reference max of each chunk's p~, per head (then its factor)
     __shared__ float2 s_MS[GMAX];             // the workgroup's max M and 1 / sum S, per head
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     f32x4 oacc[DTILES];
 #pragma unroll
     for (int n = 0; n < DTILES; ++n) oacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // p~ of chunks RLDS.. RFULL - 1 in registers (half pairs); a wave's
+    // p~ of chunks RLDS.. RFULL - 1 in registers (bfloat16 pairs); a wave's
     // chunk RFULL exists only as the last chunk of a cache with more than
     // RW * RFULL full chunks, which has at most VT keys: one 32-key tile.
     uint32_t pst[RFULL - RLDS][2 * PAIRS];
@@ -394,8 +394,8 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         uint32_t pk[2 * PAIRS];
 #pragma unroll
         for (int u = 0; u < PAIRS; ++u) {
-            pk[2 * u] = pack_f16x2(sp[u][0], sp[u][1]);
-            pk[2 * u + 1] = pack_f16x2(sp[u][2], sp[u][3]);
+            pk[2 * u] = pack_bf16x2(sp[u][0], sp[u][1]);
+            pk[2 * u + 1] = pack_bf16x2(sp[u][2], sp[u][3]);
         }
         if (k < RLDS) {
             // written as [key][head] rows now, while the wave waits for memory
@@ -459,7 +459,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     }
 
     // ---- each key's sum over this KV head's query heads of p_hj ----
-    // Every chunk's p~ ends up as [slot(key)][head] half-precision rows: the
+    // Every chunk's p~ ends up as [slot(key)][head] bfloat16 rows: the
     // LDS-resident chunks were written so in the loop, the register-held ones
     // are written to the wave's (now free) tile buffer here.  Each lane then
     // reads two keys' rows and forms sum_h p~_h * f_h with f_h =
@@ -507,16 +507,14 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         const float fk[GMAX] = {fa.x, fa.y, fa.z, fa.w, fb.x, fb.y, fb.z, fb.w};
         const int kk = chunk_of(k) * CHUNK + 2 * lane;  // the lane's first key in the item
         if (split) {
-            // each key's row of p~ f_h (relative to the part's max), half precision
+            // each key's row of p~ f_h (relative to the part's max), bfloat16
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
                 const uint4 rw = *reinterpret_cast<const uint4*>(rows + pslot(2 * lane + e) * GMAX);
                 const uint32_t wd[4] = {rw.x, rw.y, rw.z, rw.w};
                 uint32_t ow[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    ow[i] = pack_f16x2(f16_to_f32(static_cast<uint16_t>(wd[i])) * fk[2 * i],
-                                       f16_to_f32(static_cast<uint16_t>(wd[i] >> 16)) * fk[2 * i + 1]);
+                for (int i = 0; i < 4; ++i) ow[i] = pack_bf16x2(bf16_lo(wd[i]) * fk[2 * i], bf16_hi(wd[i]) * fk[2 * i + 1]);
                 if (kk + e < NK)
                     *reinterpret_cast<uint4*>(prow + static_cast<size_t>(kk + e) * GMAX) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
             }
@@ -528,8 +526,7 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
                 const uint32_t wd[4] = {rw.x, rw.y, rw.z, rw.w};
                 float acc = 0.f;
 #pragma unroll
-                for (int h = 0; h < GMAX; ++h)
-                    acc = fmaf(f16_to_f32(static_cast<uint16_t>(wd[h >> 1] >> (16 * (h & 1)))), fk[h], acc);
+                for (int h = 0; h < GMAX; ++h) acc = fmaf((h & 1) ? bf16_hi(wd[h >> 1]) : bf16_lo(wd[h >> 1]), fk[h], acc);
                 y[e] = acc;
             }
             if constexpr (RAG) {
@@ -660,7 +657,7 @@ __global__ __launch_bounds__(RFOLD_KEYS) void range_fold_parts_kernel(const Fuse
             const uint32_t wd[4] = {rw[g].x, rw[g].y, rw[g].z, rw[g].w};
 #pragma unroll
             for (int h = 0; h < GMAX; ++h)
-                acc = fmaf(f16_to_f32(static_cast<uint16_t>(wd[h >> 1] >> (16 * (h & 1)))), s_f[g * GMAX + h], acc);
+                acc = fmaf((h & 1) ? bf16_hi(wd[h >> 1]) : bf16_lo(wd[h >> 1]), s_f[g * GMAX + h], acc);
         }
     }
     const float a_old = j < len ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot

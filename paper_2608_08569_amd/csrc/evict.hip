@@ -173,7 +173,8 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh,
             float av[B];
 #pragma unroll
             for (int b = 0; b < B; ++b) {
-                const int j = min(tid + b * kSel, len - 1);
+                // clamped into the slots: slot 0 exists even when len = 0 (cap >= 1)
+                const int j = min(tid + b * kSel, max(len - 1, 0));
                 pv[b] = P[j];
                 av[b] = A[j];
             }

@@ -7,65 +7,75 @@ import pytest
 
 import oracle
 import synth
-from vzt import RTOL, GpuCache, check_close, from_dev, to_dev, widen
+from vzt import RTOL, GpuCache, check_close, check_rel, from_dev, to_dev, widen
 
 pytestmark = pytest.mark.gpu
 
 
 def synced_step(g, q, kn, vn, gamma, layers=None):
-    """One GPU step checked against the oracle on ``layers`` (all by default)."""
-    t = __import__("torch")
-    K, V, S, P = g.snapshot()
-    ls = slice(None) if layers is None else layers
+    """One GPU step checked against the oracle on ``layers`` (all by default).
+    Only those layers are copied to the host; returns the oracle's scores and
+    the GPU's state after the step, both for those layers."""
+    sel = list(range(g.L)) if layers is None else list(layers)
+    K, V, S, P = g.snapshot(sel)
     n0 = g.len
-    ref_o, ref_s, ref_p, _ = oracle.decode_step(q[ls], kn[ls], vn[ls], K[ls], V[ls], S[ls].astype(np.float64),
-                                                P[ls], n0, g.next_pos, gamma, g.dtype)
+    ref_o, ref_s, ref_p, _ = oracle.decode_step(q[sel], kn[sel], vn[sel], K, V, S.astype(np.float64), P, n0,
+                                                g.next_pos, gamma, g.dtype)
     g.step(to_dev(q), to_dev(kn), to_dev(vn), gamma)
-    K2, V2, S2, P2 = g.snapshot()
-    o = from_dev(g.out)
+    K2, V2, S2, P2 = g.snapshot(sel)
+    o = from_dev(g.out)[sel]
     rt = RTOL[g.dtype]
-    check_close(widen(o[ls], g.dtype), ref_o, rt, "attention output")
-    check_close(S2[ls][:, : n0 + 1], ref_s, rt, "decayed score")
-    assert np.array_equal(P2[ls][:, : n0 + 1], ref_p)
-    assert np.array_equal(K2[:, :, n0], kn) and np.array_equal(V2[:, :, n0], vn)   # Eq. 1 append
+    check_close(widen(o, g.dtype), ref_o, rt, "attention output")
+    check_rel(S2[:, : n0 + 1], ref_s, rt, "decayed score")
+    assert np.array_equal(P2[:, : n0 + 1], ref_p)
+    assert np.array_equal(K2[:, :, n0], kn[sel]) and np.array_equal(V2[:, :, n0], vn[sel])   # Eq. 1 append
     assert np.array_equal(K2[:, :, :n0], K[:, :, :n0]) and np.array_equal(V2[:, :, :n0], V[:, :, :n0])
     return ref_s, (K2, V2, S2, P2)
 
 
 def synced_evict(g, ref_s, state, budget, layers=None):
-    """Evict on the oracle's float32 scores; kept set bit-exact, rows position-keyed."""
+    """Evict on the oracle's float32 scores (written into the GPU state for the
+    checked layers; the other layers keep the GPU's own); on the checked
+    layers the kept set is bit-exact and the rows position-keyed."""
     t = __import__("torch")
+    sel = list(range(g.L)) if layers is None else list(layers)
     K2, V2, S2, P2 = state
-    ls = slice(None) if layers is None else layers
     T = g.len
     sc32 = S2.copy()
-    sc32[ls, :T] = ref_s.astype(np.float32)
-    g.score.copy_(t.from_numpy(sc32))
-    keep, nl = oracle.evict_select(sc32[ls].astype(np.float64), P2[ls], T, budget, 4, -1, g.next_pos)
+    sc32[:, :T] = ref_s.astype(np.float32)
+    idx = t.tensor(sel, dtype=t.long, device="cuda")
+    g.score.index_copy_(0, idx, t.from_numpy(sc32).cuda())
+    keep, nl = oracle.evict_select(sc32.astype(np.float64), P2, T, budget, 4, -1, g.next_pos)
     kept = t.full((g.L, budget), -1, dtype=t.int32, device="cuda")
     new_len = g.evict(budget, kept=kept)
     assert new_len == nl == min(T, budget)
-    K3, V3, S3, P3 = g.snapshot()
-    kept = from_dev(kept)[ls]
-    Pl = P2[ls]
-    for i in range(keep.shape[0]):
-        ref_pos = Pl[i][keep[i]]
+    K3, V3, S3, P3 = g.snapshot(sel)
+    kept = from_dev(kept)[sel]
+    for i in range(len(sel)):
+        ref_pos = P2[i][keep[i]]
         assert np.array_equal(kept[i, :nl], ref_pos), "kept position set"
-        order = np.argsort(P3[ls][i, :nl], kind="stable")
-        assert np.array_equal(P3[ls][i, :nl][order], ref_pos)
-        assert np.array_equal(K3[ls][i][:, :nl][:, order], K2[ls][i][:, keep[i]])
-        assert np.array_equal(V3[ls][i][:, :nl][:, order], V2[ls][i][:, keep[i]])
-        assert np.array_equal(S3[ls][i, :nl][order], sc32[ls][i, keep[i]])
+        order = np.argsort(P3[i, :nl], kind="stable")
+        assert np.array_equal(P3[i, :nl][order], ref_pos)
+        assert np.array_equal(K3[i][:, :nl][:, order], K2[i][:, keep[i]])
+        assert np.array_equal(V3[i][:, :nl][:, order], V2[i][:, keep[i]])
+        assert np.array_equal(S3[i, :nl][order], sc32[i, keep[i]])
+    return T - nl
 
 
 def _run_workload(w, g, steps, start_step=0, layers=None, budget=None, interval=1):
+    """Steps (with the eviction rule of Sec. 3.2.2: after the score update,
+    every `interval` steps, when len > B) state-synced against the oracle;
+    returns the number of evictions and of rows they removed."""
     budget = w.budget if budget is None else budget
     bias = synth.q_bias(w) if w.q_bias else None
+    n_ev = rows = 0
     for t in range(start_step, start_step + steps):
         q, kn, vn = synth.decode_inputs(w, t, bias=bias)
         ref_s, state = synced_step(g, q, kn, vn, w.gamma, layers)
         if (t + 1) % interval == 0 and g.len > budget:
-            synced_evict(g, ref_s, state, budget, layers)
+            rows += synced_evict(g, ref_s, state, budget, layers)
+            n_ev += 1
+    return n_ev, rows
 
 
 def test_tiny_fused_no_eviction_needed():
@@ -216,16 +226,22 @@ def test_deterministic_bits():
 
 
 def test_long32k_full_size_sampled_layers():
-    """The 48-layer 32k-token workload at full size: fuse, then decode steps with
-    eviction; layers 0 and 47 are checked against the oracle every step."""
+    """The 48-layer 32k-token workload at full size: fuse (8,150 spans), then
+    decode steps until the cache has crossed the budget B = 8192 and been
+    evicted for several steps (one row per layer and step, T = 8193: the
+    steady state that bench.py times); layers 0, 23 and 47 are checked against
+    the oracle at every step and every eviction."""
     w = synth.workload("long32k")
     off = synth.offsets_from_lengths(synth.span_lengths(w))
     n = len(off) - 1
+    assert n < w.budget
+    steps = w.budget - n + 8          # the last 8 steps each evict one row
     cap = max(n, w.budget) + 32
     g = GpuCache(w.n_layers, w.n_q_heads, w.kv_heads, w.d, cap, w.dtype)
     g.fuse(to_dev(synth.prefill_kv(w, "k")), to_dev(synth.prefill_kv(w, "v")), to_dev(off))
-    _run_workload(w, g, 6, layers=[0, 47])
-    assert g.len == min(n + 6, w.budget) or g.len == w.budget
+    n_ev, rows = _run_workload(w, g, steps, layers=[0, 23, 47])
+    assert (n_ev, rows) == (8, 8)
+    assert g.len == w.budget
 
 
 def test_aggr64k_full_size_sampled_layers():
@@ -311,5 +327,5 @@ def test_concurrent_calls_on_separate_streams():
             S[:, : n + t + 1] = rs
             P[:, : n + t + 1] = rp
         check_close(widen(from_dev(g.out), dtype), ro, RTOL[dtype], f"sequence {i} output")
-        check_close(from_dev(g.score)[:, : n + 3], S[:, : n + 3], RTOL[dtype], f"sequence {i} score")
+        check_rel(from_dev(g.score)[:, : n + 3], S[:, : n + 3], RTOL[dtype], f"sequence {i} score")
         assert np.array_equal(from_dev(g.pos)[:, : n + 3], P[:, : n + 3])

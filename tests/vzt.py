@@ -54,6 +54,26 @@ def check_close(got: np.ndarray, ref: np.ndarray, rtol: float, what: str = "") -
     return worst
 
 
+def check_rel(got: np.ndarray, ref: np.ndarray, rtol: float, what: str = "") -> float:
+    """|got - ref| <= rtol*|ref|, element by element: the bound for the decayed
+    scores, which are non-negative, so that the smallest ones (the slots
+    Eq. (9) evicts) are held to their own size.  Returns the largest error in
+    units of the allowed error."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    if ref.size == 0:
+        return 0.0
+    allow = rtol * np.abs(ref) + 1e-38
+    err = np.abs(got - ref)
+    worst = float(np.max(err / allow))
+    if worst > 1.0:
+        idx = np.unravel_index(np.argmax(err / allow), err.shape)
+        raise AssertionError(f"{what}: element {idx} got {got[idx]!r} ref {ref[idx]!r} "
+                             f"(err {err[idx]:.3g}, allowed {allow[idx]:.3g})")
+    return worst
+
+
 def bf16_ulp(x: np.ndarray) -> np.ndarray:
     ax = np.maximum(np.abs(x), 2.0 ** -126)
     return 2.0 ** (np.floor(np.log2(ax)) - 7)
@@ -94,9 +114,14 @@ class GpuCache:
         self.pos.copy_(t.from_numpy(np.ascontiguousarray(pos, dtype=np.int32)))
         self.len, self.next_pos = length, next_pos
 
-    def snapshot(self):
+    def snapshot(self, layers=None):
+        """Host copies of K, V, score and pos: every layer, or the listed ones
+        (gathered on the device first, so a long cache pulls only those)."""
         torch().cuda.synchronize()
-        return (from_dev(self.k), from_dev(self.v), from_dev(self.score), from_dev(self.pos))
+        if layers is None:
+            return (from_dev(self.k), from_dev(self.v), from_dev(self.score), from_dev(self.pos))
+        idx = torch().tensor(list(layers), dtype=torch().long, device="cuda")
+        return tuple(from_dev(x.index_select(0, idx)) for x in (self.k, self.v, self.score, self.pos))
 
     def step(self, q_dev, k_dev, v_dev, gamma, sm_scale=0.0, check_ws=True):
         self.vz.voxzip_decode_attend_score(q_dev, k_dev, v_dev, self.k, self.v, self.score, self.pos, self.out,
