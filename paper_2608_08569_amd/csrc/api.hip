@@ -224,7 +224,8 @@ int voxzip_decode_attend_score(const void* q, const void* k_new, const void* v_n
     const size_t need = vz_decode_ws_bytes(n_layers, n_q_heads, kv_heads, d, cap, 0);
     if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     VzDecodeArgs a{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
-                   n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, ws_bytes, VzRagged{}};
+                   n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, ws_bytes, VzRagged{},
+                   0, 0, 0, 0, nullptr, nullptr};
     hipError_t e = vz_launch_decode(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
 }
@@ -274,20 +275,22 @@ int voxzip_decode_evict(const void* q, const void* k_new, const void* v_new, voi
     if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     hipStream_t st = static_cast<hipStream_t>(stream);
     VzDecodeArgs da{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
-                    n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, split, VzRagged{}};
+                    n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, split, VzRagged{},
+                    0, 0, 0, 0, nullptr, nullptr};
     void* ews = static_cast<uint8_t*>(workspace) + split;
     VzEvictArgs ea{k_cache, v_cache, score, pos, T, budget, n_sink, M, next_pos + 1, kept_pos_out,
                    n_layers, kv_heads, d, cap, dtype, ews, ws_bytes - split, VzRagged{}, nullptr};
     const bool evict = T > budget || kept_pos_out != nullptr;
     hipError_t e;
-    if (evict && vz_decode_takes_range(da) && vz_fold_evict_ok(dtype, d, kv_heads, T, budget)) {
-        // whole-range decode without its fold launch, then fold + select in one
-        da.range_no_fold = 1;
+    if (evict && vz_decode_evicts(da, budget)) {
+        // one launch: the decode kernel's last workgroup per layer folds and evicts
+        da.ev = 1;
+        da.ev_budget = budget;
+        da.ev_sink = n_sink;
+        da.ev_M = M;
+        da.ev_kept = kept_pos_out;
+        da.ev_n = static_cast<int32_t*>(ews);  // the eviction workspace's move counts
         e = vz_launch_decode(da, st);
-        if (e == hipSuccess)
-            e = vz_launch_fold_evict(ea, reinterpret_cast<const float*>(static_cast<uint8_t*>(workspace) +
-                                                                         vz_decode_hdr_bytes(n_layers)),
-                                     vz_range_sum_row(cap), gamma, st);
     } else {
         e = vz_launch_decode(da, st);
         if (e == hipSuccess && evict) e = vz_launch_evict(ea, st);
@@ -358,7 +361,8 @@ int voxzip_decode_attend_score_ragged(const void* q, const void* k_new, const vo
     if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     VzRagged rg{seq_base, cap, len, next_pos, nullptr, status, n_seqs, total};
     VzDecodeArgs a{q,  k_new, v_new, k_cache, v_cache, score, pos,   out,       0,        0,  gamma, sm_scale,
-                   n_layers, n_q_heads, kv_heads, d, 0, dtype, workspace, ws_bytes, rg};
+                   n_layers, n_q_heads, kv_heads, d, 0, dtype, workspace, ws_bytes, rg,
+                   0, 0, 0, 0, nullptr, nullptr};
     hipError_t e = vz_launch_decode(a, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
 }

@@ -33,9 +33,12 @@
 // partials, and the layer's (max, sum) of the head.  Fold kernel: per (chunk,
 // layer), the chunk's scores A[j] = gamma A[j] + sum_h p_hj from p~ and one
 // factor per head.
+#include <atomic>
+#include <random>
 #include <type_traits>
 
 #include "decode_mfma.h"
+#include "select.h"
 
 namespace {
 
@@ -43,7 +46,10 @@ using namespace vz_mfma;
 
 constexpr int ATTEND_WG_PER_CU = 4;  // resident attend workgroups per CU (128 VGPRs)
 constexpr int ATTEND_DEEP_MAX_ITEMS = 512;  // attend grids this small keep four tiles in flight per wave
-constexpr size_t kHeaderBytes = 256;  // decode workspace header (unused by this path)
+// Decode workspace header: 256 reserved bytes (a ragged call keeps its table
+// sizes there), then one arrival counter per layer (whole-range path, zero
+// after every call), padded to 256 bytes.
+constexpr size_t kHeaderBytes = 256;
 
 // Per-chunk partial results in the workspace, after the header:
 //   ml [L][nc_max][Hq]        float2     chunk max m_c and sum l_c of exp2, per head
@@ -666,7 +672,19 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
         a.n_chunks = static_cast<int32_t>((static_cast<int64_t>(v.len) + CHUNK) / CHUNK);  // of len + 1 keys
         a.nc_max = static_cast<int32_t>(chunk_rows(a.plane, 0));
     }
-    if (vz_decode_range_ok(a.L, NW, RAG ? v.rag.n : 0)) return vz_launch_decode_range(a, NW, !v.range_no_fold, stream);
+    if (vz_decode_range_ok(a.L, NW, RAG ? v.rag.n : 0)) {
+        if (!RAG) {
+            a.cnt = reinterpret_cast<uint64_t*>(a.ws + kHeaderBytes);
+            a.tag = vz_call_tag();
+            a.ev = v.ev;
+            a.ev_budget = v.ev_budget;
+            a.ev_sink = v.ev_sink;
+            a.ev_M = v.ev_M;
+            a.ev_kept = v.ev_kept;
+            a.ev_n = v.ev_n;
+        }
+        return vz_launch_decode_range(a, NW, stream);
+    }
     // grids of at most two workgroups per CU: four tiles in flight per wave
     // (all eight measured slower: their registers spill into the AGPRs)
     if (static_cast<int64_t>(a.L) * a.n_chunks <= ATTEND_DEEP_MAX_ITEMS)
@@ -696,8 +714,15 @@ hipError_t launch_decode_fused_any(const VzDecodeArgs& v, hipStream_t stream) {
 
 // ---- sizing shared with the host API ----
 size_t vz_decode_hdr_bytes(int32_t L) {
-    (void)L;
-    return kHeaderBytes;
+    return kHeaderBytes + (static_cast<size_t>(L) * sizeof(uint64_t) + 255) / 256 * 256;
+}
+
+uint32_t vz_call_tag() {
+    static std::atomic<uint32_t> next{static_cast<uint32_t>(std::random_device{}())};
+    uint32_t t;
+    do t = next.fetch_add(1, std::memory_order_relaxed);
+    while (t == 0);
+    return t;
 }
 
 bool vz_decode_fused_ok(int32_t dtype, int32_t d, int32_t Hq, int32_t Hkv, int32_t L, int64_t plane, int32_t n_seqs) {
@@ -728,4 +753,10 @@ hipError_t vz_launch_decode_fused(const VzDecodeArgs& a, hipStream_t stream) {
 bool vz_decode_takes_range(const VzDecodeArgs& a) {
     return a.rag.n == 0 && vz_decode_fused_ok(a.dtype, a.d, a.Hq, a.Hkv, a.L, a.cap, 0) &&
            vz_decode_range_ok(a.L, a.Hkv, 0) && vz_decode_range_whole(a.len);
+}
+
+bool vz_decode_evicts(const VzDecodeArgs& a, int32_t budget) {
+    const int64_t T = static_cast<int64_t>(a.len) + 1;
+    const int64_t E = T > budget ? T - budget : 0;
+    return vz_decode_takes_range(a) && a.Hkv <= 4 && E <= vz_sel::kInlineRows;
 }

@@ -92,6 +92,17 @@ struct FusedArgs {
     // every key; else parts of part_keys keys, the last one shorter), and the
     // bounds of a ragged call's work tables (R parts, FB fold blocks)
     int32_t n_parts, part_keys, R, FB;
+    // whole-range path, a single sequence in one part: the last workgroup of
+    // each layer to finish (elected on the arrival counters cnt[L] with the
+    // call's tag) folds the scores (Eq. 6) and, when ev != 0, runs the
+    // eviction of the len + 1 slots (Sec. 3.2.2 Eq. 7-9) with budget ev_budget,
+    // ev_sink sinks, an ev_M recent window, optional kept positions ev_kept
+    // [L][ev_budget] and the move counts ev_n [L] of the eviction workspace
+    uint64_t* cnt;
+    uint32_t tag;
+    int32_t ev, ev_budget, ev_sink, ev_M;
+    int32_t* ev_kept;
+    int32_t* ev_n;
 };
 
 }  // namespace vz_mfma
@@ -100,7 +111,7 @@ struct FusedArgs {
 // heads and n_seqs sequences (0: a single sequence) takes it, and its
 // launches (a single sequence: a.len, a.next_pos; a ragged batch: a.rag).
 bool vz_decode_range_ok(int32_t L, int32_t Hkv, int32_t n_seqs);
-hipError_t vz_launch_decode_range(const vz_mfma::FusedArgs& a, int32_t Hkv, bool fold, hipStream_t stream);
+hipError_t vz_launch_decode_range(const vz_mfma::FusedArgs& a, int32_t Hkv, hipStream_t stream);
 // Whether a single sequence of len resident keys is one part (one launch of
-// the range kernel leaving the head-group sums, then the fold).
+// the range kernel, which also folds the scores, and evicts when asked).
 bool vz_decode_range_whole(int32_t len);

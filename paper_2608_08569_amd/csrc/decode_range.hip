@@ -5,6 +5,7 @@
 // Compiled with the max-ILP machine scheduler (per-file flag of the build):
 // the default one over-subscribes the 256 registers per lane and spills.
 #include "decode_mfma.h"
+#include "select.h"
 
 namespace {
 
@@ -26,8 +27,11 @@ using namespace vz_mfma;
 // m_ref it was taken against.  At the end
 // the waves merge their (max, sum) pairs and outputs in LDS, the workgroup
 // writes its query heads' output rows, and every key's sum over those heads
-// of p_hj goes to the workspace.  A fold kernel then adds the KV heads' sums
-// into Eq. (6).  A part of a longer sequence instead leaves its statistics,
+// of p_hj goes to the workspace.  For a sequence in one part, the last of a
+// layer's workgroups to finish then adds the KV heads' sums into Eq. (6) and,
+// in a generation step, runs the eviction of Sec. 3.2.2 for the layer (see
+// arrive_last); no workgroup ever waits for another.  For ragged calls a fold
+// kernel adds the sums.  A part of a longer sequence instead leaves its statistics,
 // output and per-head probabilities relative to its own max, which a merge
 // kernel and the fold combine.  Compared with the chunked path there are no
 // per-chunk partial outputs or probabilities in HBM; it needs enough (layer,
@@ -179,6 +183,27 @@ __device__ __forceinline__ RangeItem uniform_item(const RangeItem& x) {
     return it;
 }
 
+// Arrival of one workgroup of a layer (thread 0, after every store the others
+// need has completed): a lock-free compare-and-swap on the layer's counter,
+// whose high word is the call's tag and whose low word counts this call's
+// arrivals.  A counter holding another tag (an earlier call, or memory never
+// used) counts as zero, so the workspace needs no initialisation.  Returns
+// true for the n-th arrival, which also resets the counter to 0 (a graph
+// replaying the call with the same tag starts from zero again).  Relaxed
+// device-scope atomics: the data the last arriver reads was written with
+// device-coherent stores that completed before the arrivals.
+__device__ __forceinline__ bool arrive_last(uint64_t* c, uint32_t tag, uint32_t n) {
+    uint64_t cur = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t want;
+    do {
+        want = (static_cast<uint32_t>(cur >> 32) == tag ? cur : static_cast<uint64_t>(tag) << 32) + 1;
+    } while (!__hip_atomic_compare_exchange_weak(c, &cur, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT));
+    const bool last = static_cast<uint32_t>(want) == n;
+    if (last) __hip_atomic_store(c, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return last;
+}
+
 // Grid (NW, L) for a sequence of one part; NW x L x items, flattened, for
 // parts and ragged calls (KV head fastest, then layer, then item, so a
 // ragged call's items go out in the table's order): workgroup (g, l, r)
@@ -186,9 +211,11 @@ __device__ __forceinline__ RangeItem uniform_item(const RangeItem& x) {
 // ragged call's table (dispatch order longest first); else the parts of the
 // single sequence.  SPLIT: items may be parts of a longer sequence, whose
 // statistics, outputs and per-head probabilities go to the workspace for the
-// merge and fold kernels.
+// merge and fold kernels.  Neither (a single sequence in one part): the
+// layer's last workgroup folds the scores and evicts (fold_select_layer).
 template <int NW, bool RAG, bool SPLIT>
 __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArgs a) {
+    constexpr bool FS = !RAG && !SPLIT;
     static_assert(RW * GMAX * RO_STRIDE * 4 <= RW * TILE_BYTES, "the merged outputs fit in the tile buffers");
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[RW][TILE_BYTES];
     __shared__ float2 s_stat[RW][GMAX];
@@ -244,7 +271,8 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
             *reinterpret_cast<uint4*>(Kh + at + 8 * lane) = *reinterpret_cast<const uint4*>(kn + 8 * lane);
         else if (lane < 32)
             *reinterpret_cast<uint4*>(Vh + at + 8 * (lane - 16)) = *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
-        if (g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
+        // (with FS the last workgroup of the layer writes the position)
+        if (!FS && g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
         __threadfence_block();
     }
 
@@ -533,30 +561,51 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
                 // slots past the item belong to the next sequence: masked
                 if (kk < NK) gsum[kk] = y[0];
                 if (kk + 1 < NK) gsum[kk + 1] = y[1];
+            } else if constexpr (FS) {
+                // device-coherent: another workgroup of this kernel folds them
+                const uint64_t pair = static_cast<uint64_t>(__float_as_uint(y[0])) |
+                                      (static_cast<uint64_t>(__float_as_uint(y[1])) << 32);
+                __hip_atomic_store(reinterpret_cast<uint64_t*>(gsum + kk), pair, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
             } else {
                 *reinterpret_cast<float2*>(gsum + kk) = make_float2(y[0], y[1]);
             }
         }
     }
-}
-
-// Fold kernel of the whole-range path, thread = key: Eq. (6) with the KV
-// heads' sums added in head order (the new slot starts from 0).
-constexpr int RFOLD_THREADS = 256;
-template <int NW>
-__global__ __launch_bounds__(RFOLD_THREADS) void decode_range_fold_kernel(const FusedArgs a) {
-    const int l = blockIdx.y;
-    const int len = a.len;
-    const int j = min(static_cast<int>(blockIdx.x) * RFOLD_THREADS + static_cast<int>(threadIdx.x), len);
-    const int64_t row = range_row(a.plane);
-    const float* gs = reinterpret_cast<const float*>(a.ws + a.hdr_bytes) + static_cast<size_t>(l) * NW * row + j;
-    float* const sc = a.score + static_cast<size_t>(l) * a.plane + j;
-    const float a_ld = *sc;
-    float acc = gs[0];
-#pragma unroll
-    for (int g = 1; g < NW; ++g) acc += gs[g * row];
-    const float a_old = j < len ? a_ld : 0.f;  // zero pad of Eq. (6) for the new slot
-    if (static_cast<int>(blockIdx.x) * RFOLD_THREADS + static_cast<int>(threadIdx.x) <= len) *sc = fmaf(a.gamma, a_old, acc);
+    if constexpr (FS) {
+        // ---- the layer's last workgroup: Eq. (6) fold, then the eviction ----
+        using Sel = vz_sel::SelShared<64 * RW, RANGE_MAX_KEYS>;
+        static_assert(sizeof(Sel) <= sizeof(s_pt), "the selection's LDS fits in the p~ rows");
+        __shared__ int s_last;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's sums have reached the device
+        __syncthreads();
+        if (tid == 0) s_last = arrive_last(a.cnt + l, a.tag, NW);
+        __syncthreads();
+        if (!s_last) return;
+        Sel& sh = *reinterpret_cast<Sel*>(&s_pt[0][0][0][0]);  // the p~ rows are no longer read
+        vz_sel::FoldLayer<uint16_t> f;
+        const size_t lrow = static_cast<size_t>(l) * a.plane;
+        f.A = a.score + lrow;
+        f.P = a.pos + lrow;
+        f.k0 = a.k_cache + lrow * NW * D;
+        f.v0 = a.v_cache + lrow * NW * D;
+        f.head_stride = static_cast<size_t>(a.plane) * D;
+        f.S = rws.sums + static_cast<size_t>(l) * NW * rws.row;
+        f.row = rws.row;
+        f.k_new = a.k_new + seq_row * NW * D;
+        f.v_new = a.v_new + seq_row * NW * D;
+        f.len = len + 1;
+        f.next_pos = it.next_pos + 1;
+        f.gamma = a.gamma;
+        f.select = a.ev != 0;
+        f.budget = a.ev_budget;
+        f.n_sink = a.ev_sink;
+        f.M = a.ev_M;
+        f.kept = a.ev_kept ? a.ev_kept + static_cast<size_t>(l) * a.ev_budget : nullptr;
+        f.n_out = a.ev_n ? a.ev_n + l : nullptr;
+        // one round of 16 or 17 slots per thread for up to 4 KV heads, rounds of 9 for 8
+        vz_sel::fold_select_layer<64 * RW, NW <= 4 ? 17 : 9, VZ_BF16, D, NW, true>(f, sh);
+    }
 }
 
 // Merge of a sequence in parts, one block per (sequence, layer) at its first
@@ -830,7 +879,7 @@ int32_t ragged_fold_bound(int32_t n_seqs, int64_t total) {
 }
 
 template <int NW>
-hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
+hipError_t launch_range(const FusedArgs& a, hipStream_t stream) {
     if (a.rag.n > 0) {
         hipLaunchKernelGGL((range_order_kernel<NW>), dim3(1), dim3(ORDER_THREADS), 0, stream, a);
         hipLaunchKernelGGL((decode_range_kernel<NW, true, true>), dim3(NW * a.L * a.R), dim3(64 * RW), 0, stream, a);
@@ -848,10 +897,6 @@ hipError_t launch_range(const FusedArgs& a, bool fold, hipStream_t stream) {
         return hipGetLastError();
     }
     hipLaunchKernelGGL((decode_range_kernel<NW, false, false>), dim3(NW, a.L), dim3(64 * RW), 0, stream, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !fold) return e;
-    hipLaunchKernelGGL((decode_range_fold_kernel<NW>), dim3((a.len + RFOLD_THREADS) / RFOLD_THREADS, a.L),
-                       dim3(RFOLD_THREADS), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -862,7 +907,7 @@ bool vz_decode_range_ok(int32_t L, int32_t Hkv, int32_t n_seqs) {
     return static_cast<int64_t>(L) * Hkv >= RANGE_MIN_ITEMS;
 }
 
-hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, bool fold, hipStream_t stream) {
+hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, hipStream_t stream) {
     FusedArgs a = a0;
     if (a.rag.n > 0) {
         a.R = ragged_items_bound(a.rag.n, a.plane);
@@ -873,10 +918,10 @@ hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, bool fold, h
         a.FB = 0;
     }
     switch (Hkv) {
-        case 1: return launch_range<1>(a, fold, stream);
-        case 2: return launch_range<2>(a, fold, stream);
-        case 4: return launch_range<4>(a, fold, stream);
-        case 8: return launch_range<8>(a, fold, stream);
+        case 1: return launch_range<1>(a, stream);
+        case 2: return launch_range<2>(a, stream);
+        case 4: return launch_range<4>(a, stream);
+        case 8: return launch_range<8>(a, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -891,4 +936,3 @@ size_t vz_decode_range_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int64_t plan
     return range_layout(vz_decode_hdr_bytes(L), L, Hkv, Hq, plane, R, FB, rag, off);
 }
 
-int64_t vz_range_sum_row(int64_t plane) { return range_row(plane); }

@@ -205,9 +205,13 @@ struct VzDecodeArgs {
     // ragged batch (rag.n > 0): len, next_pos and cap above are unused; q, out
     // are [n][L][Hq][d], k_new, v_new [n][L][Hkv][d], planes hold rag.total slots
     VzRagged rag;
-    // whole-range path only: leave the head-group sums in the workspace and
-    // skip the fold launch (a fused fold + eviction follows)
-    int32_t range_no_fold;
+    // a single sequence on the whole-range path in one part
+    // (vz_decode_evicts): the eviction of the len + 1 slots the step leaves
+    // runs in the decode kernel (ev = 1), with these arguments; ev_n is the
+    // eviction workspace's move-count array
+    int32_t ev, ev_budget, ev_sink, ev_M;
+    int32_t* ev_kept;
+    int32_t* ev_n;
 };
 
 struct VzEvictArgs {
@@ -256,17 +260,14 @@ bool vz_decode_generic_ok(int64_t plane, int32_t n_seqs);
 size_t vz_decode_generic_ws_bytes(int32_t L, int32_t Hq, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_decode_generic(const VzDecodeArgs& a, hipStream_t stream);
 hipError_t vz_launch_decode(const VzDecodeArgs& a, hipStream_t stream);
-// Whole-range decode path (single sequence): whether a call takes it, and
-// where it leaves the KV heads' head-group sums ([L][Hkv][row] floats right
-// after the workspace header).
+// Whole-range decode path (single sequence): whether a call takes it.
 bool vz_decode_takes_range(const VzDecodeArgs& a);
-int64_t vz_range_sum_row(int64_t plane);
 // Workspace of the whole-range path (single sequence or ragged batch).
 size_t vz_decode_range_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int64_t plane, int32_t n_seqs);
-// Score fold of a whole-range decode fused with the eviction that follows
-// (bf16, d = 128, Hkv <= 4, the keys in LDS, at most 256 moved rows).
-bool vz_fold_evict_ok(int32_t dtype, int32_t d, int32_t Hkv, int32_t len, int32_t budget);
-hipError_t vz_launch_fold_evict(const VzEvictArgs& a, const float* sums, int64_t row, float gamma,
-                                hipStream_t stream);
+// Whether a decode call's kernel also runs the eviction of the len + 1 slots
+// it leaves (whole-range path in one part, Hkv <= 4, at most 256 moved rows).
+bool vz_decode_evicts(const VzDecodeArgs& a, int32_t budget);
+// A fresh nonzero tag per call (arrival counters of the whole-range path).
+uint32_t vz_call_tag();
 size_t vz_evict_ws_bytes(int32_t L, int64_t plane, int32_t n_seqs);
 hipError_t vz_launch_evict(const VzEvictArgs& a, hipStream_t stream);

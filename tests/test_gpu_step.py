@@ -11,7 +11,7 @@ import pytest
 
 import synth
 from test_gpu_range import layered_state, step_inputs
-from vzt import from_dev, to_dev
+from vzt import decode_header_bytes, from_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -64,8 +64,8 @@ def test_step_equals_decode_then_evict(Hq, Hkv, L, length, budget, dtype, d, kep
         assert np.array_equal(from_dev(a[name]), from_dev(b[name])), name
     if kept:
         assert np.array_equal(from_dev(kept_a), from_dev(kept_b))
-    hdr = from_dev(ws[:256])
-    assert not hdr.any()  # the decode part's reserved header is left zero
+    hdr = from_dev(ws[:decode_header_bytes(L)])
+    assert not hdr.any()  # the decode part's header (reserved bytes, arrival counters) is left zero
 
 
 def test_steps_in_a_row():
@@ -94,3 +94,80 @@ def test_steps_in_a_row():
         for name in ("out", "k", "v", "score", "pos"):
             assert np.array_equal(from_dev(a[name]), from_dev(b[name])), (t, name)
         length, next_pos = n_a, next_pos + 1
+
+
+@pytest.mark.parametrize("length,budget", [(8192, 8192), (8195, 8190), (3000, 5000)])
+def test_uninitialised_workspace(length, budget):
+    """A workspace full of random bytes (never zeroed) gives the bits of a
+    zeroed one: the per-layer arrival counters carry the call's tag, so
+    whatever they held before counts as no arrivals."""
+    import torch
+    import paper_2608_08569_amd as vz
+    L, Hq, Hkv, d, dt = 48, 32, 4, 128, synth.DT_BF16
+    cap = length + 2
+    a, b = _state(L, Hq, Hkv, d, cap, length, dt, seed=45)
+    q, kn, vn = (to_dev(x) for x in step_inputs(synth.stream_key(45, "noinit", length), 0, L, Hq, Hkv, d, dt))
+    ws0 = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(46)
+    ws1 = torch.randint(0, 256, ws0.shape, dtype=torch.uint8, device="cuda", generator=g)
+    for x, ws in ((a, ws0), (b, ws1)):
+        vz.voxzip_decode_evict(q, kn, vn, x["k"], x["v"], x["score"], x["pos"], x["out"], length, length + 9, 0.95,
+                               budget, workspace=ws)
+    torch.cuda.synchronize()
+    for name in ("out", "k", "v", "score", "pos"):
+        assert np.array_equal(from_dev(a[name]), from_dev(b[name])), name
+    # the counters are left at zero either way
+    assert not from_dev(ws1[256:256 + 8 * L]).any()
+
+
+def test_graph_replay_of_the_generation_step():
+    """One generation step (decode + fold + eviction in one kernel) captured
+    in a HIP graph and replayed 6 times (every replay reuses the captured
+    tag: the counters must be back at zero after each), with eager work and
+    synchronisations between the replays; every replay equals an eager call
+    on the same state, bit for bit."""
+    import torch
+    import paper_2608_08569_amd as vz
+    L, Hq, Hkv, d, dt, length, budget = 48, 32, 4, 128, synth.DT_BF16, 4096, 4096
+    cap = length + 2
+    a, b = _state(L, Hq, Hkv, d, cap, length, dt, seed=47)
+    ins = [[to_dev(x) for x in step_inputs(synth.stream_key(47, "graph"), t, L, Hq, Hkv, d, dt)] for t in range(6)]
+    qb, kb, vb = (torch.zeros_like(x) for x in ins[0])
+    ws_a = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+    ws_b = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+    nxt = length + 9
+    # the replayed step always starts at len = budget (it evicts one row), so
+    # the captured call's scalar arguments stay valid; positions advance by
+    # rewriting the new token's position argument is not possible, so each
+    # replay restarts from the same next_pos on a state copied back in
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(st):
+        vz.voxzip_decode_evict(qb, kb, vb, a["k"], a["v"], a["score"], a["pos"], a["out"], length, nxt, 0.95, budget,
+                               workspace=ws_a, stream=st)  # warm-up outside the capture
+    torch.cuda.synchronize()
+    a2, _ = _state(L, Hq, Hkv, d, cap, length, dt, seed=47)
+    for name in a:
+        a[name].copy_(a2[name])
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=st):
+        vz.voxzip_decode_evict(qb, kb, vb, a["k"], a["v"], a["score"], a["pos"], a["out"], length, nxt, 0.95, budget,
+                               workspace=ws_a, stream=st)
+    for t in range(6):
+        for name in a:
+            a[name].copy_(a2[name])
+            b[name].copy_(a2[name])
+        qb.copy_(ins[t][0])
+        kb.copy_(ins[t][1])
+        vb.copy_(ins[t][2])
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        vz.voxzip_decode_evict(ins[t][0], ins[t][1], ins[t][2], b["k"], b["v"], b["score"], b["pos"], b["out"],
+                               length, nxt, 0.95, budget, workspace=ws_b)
+        torch.cuda.synchronize()
+        for name in ("out", "k", "v", "score", "pos"):
+            assert np.array_equal(from_dev(a[name]), from_dev(b[name])), (t, name)
+        assert not from_dev(ws_a[256:256 + 8 * L]).any()

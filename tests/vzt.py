@@ -74,6 +74,12 @@ def check_rel(got: np.ndarray, ref: np.ndarray, rtol: float, what: str = "") -> 
     return worst
 
 
+def decode_header_bytes(L: int) -> int:
+    """Bytes of a decode workspace's header: 256 reserved bytes, then one
+    8-byte arrival counter per layer, padded to 256 bytes."""
+    return 256 + (8 * L + 255) // 256 * 256
+
+
 def bf16_ulp(x: np.ndarray) -> np.ndarray:
     ax = np.maximum(np.abs(x), 2.0 ** -126)
     return 2.0 ** (np.floor(np.log2(ax)) - 7)
@@ -137,11 +143,13 @@ class GpuCache:
         return self.dtype == synth.DT_BF16 and self.d == 128 and self.Hkv in (1, 2, 4, 8) and G <= 8
 
     def check_decode_workspace(self):
-        """After every call the decode workspace's reserved header is still
-        zero (no kernel writes outside its partial-result rows)."""
+        """After every call the decode workspace's header is still zero: its
+        256 reserved bytes (no kernel writes outside its partial-result rows)
+        and the per-layer arrival counters after them (the last workgroup of
+        each layer resets its counter)."""
         torch().cuda.synchronize()
-        hdr = from_dev(self.ws_dec[:256]).view(np.uint32)
-        assert not hdr.any(), f"decode workspace header not zero: {hdr[:4]}"
+        hdr = from_dev(self.ws_dec[:decode_header_bytes(self.L)]).view(np.uint32)
+        assert not hdr.any(), f"decode workspace header not zero at word {np.flatnonzero(hdr)[:4]}"
 
     def evict(self, budget, n_sink=4, n_recent=-1, kept=None):
         self.len = self.vz.voxzip_evict_compact(self.k, self.v, self.score, self.pos, self.len, budget,
