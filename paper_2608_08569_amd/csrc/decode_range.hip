@@ -445,6 +445,17 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         }
     }
 
+    // The layer's old scores and positions for the fold of its last
+    // workgroup, in flight during the epilogue (loads are counted in order
+    // with the stores, so issued here they are back before the arrival waits
+    // for the head-group sums' stores).
+    constexpr int FB = (RANGE_MAX_KEYS + 64 * RW - 1) / (64 * RW);        // slots per thread
+    constexpr int FR = (RANGE_MAX_KEYS + 4 * 64 * RW - 1) / (4 * 64 * RW);  // rounds of 4 slots per thread
+    vz_sel::FoldOld<FB> old;
+    if constexpr (FS)
+        vz_sel::fold_prefetch<64 * RW, FB>(a.score + static_cast<size_t>(l) * a.plane,
+                                            a.pos + static_cast<size_t>(l) * a.plane, len + 1, old);
+
     // ---- the workgroup's statistics per head: max M and 1 / sum ----
     if (q4 == 0 && hi == 0) s_stat[w][hh] = make_float2(m_w, l_w);
     __syncthreads();
@@ -574,15 +585,10 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     }
     if constexpr (FS) {
         // ---- the layer's last workgroup: Eq. (6) fold, then the eviction ----
-        using Sel = vz_sel::SelShared<64 * RW, RANGE_MAX_KEYS>;
+        using Sel = vz_sel::SelShared<64 * RW, FB * 64 * RW>;
         static_assert(sizeof(Sel) <= sizeof(s_pt), "the selection's LDS fits in the p~ rows");
+        static_assert((4 * FR + 2) * 64 * RW * 4 <= sizeof(s_tile) && FB <= 4 * FR, "the summed sums fit in the tiles");
         __shared__ int s_last;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's sums have reached the device
-        __syncthreads();
-        if (tid == 0) s_last = arrive_last(a.cnt + l, a.tag, NW);
-        __syncthreads();
-        if (!s_last) return;
-        Sel& sh = *reinterpret_cast<Sel*>(&s_pt[0][0][0][0]);  // the p~ rows are no longer read
         vz_sel::FoldLayer<uint16_t> f;
         const size_t lrow = static_cast<size_t>(l) * a.plane;
         f.A = a.score + lrow;
@@ -603,8 +609,14 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         f.M = a.ev_M;
         f.kept = a.ev_kept ? a.ev_kept + static_cast<size_t>(l) * a.ev_budget : nullptr;
         f.n_out = a.ev_n ? a.ev_n + l : nullptr;
-        // one round of 16 or 17 slots per thread for up to 4 KV heads, rounds of 9 for 8
-        vz_sel::fold_select_layer<64 * RW, NW <= 4 ? 17 : 9, VZ_BF16, D, NW, true>(f, sh);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's sums have reached the device
+        __syncthreads();
+        if (tid == 0) s_last = arrive_last(a.cnt + l, a.tag, NW);
+        __syncthreads();
+        if (!s_last) return;
+        Sel& sh = *reinterpret_cast<Sel*>(&s_pt[0][0][0][0]);             // the p~ rows are no longer read
+        float* const s_acc = reinterpret_cast<float*>(&s_tile[0][0]);      // nor the tiles
+        vz_sel::fold_select_layer<64 * RW, FB, FR, VZ_BF16, D, NW>(f, old, s_acc, sh);
     }
 }
 

@@ -51,21 +51,28 @@ struct SelShared {
     int32_t ev[kSmallE];     // slots of the evicted keys found by the rounds (keys in LDS only)
     int32_t holes[kSmallE];  // those below the budget, ascending
     int nm;
-    float pre_a[kSmallE];    // fused fold: new score and position of the slots at or past the budget
-    int32_t pre_p[kSmallE];
     int32_t src[kInlineRows], dst[kInlineRows];  // move lists (keys in LDS only)
     uint64_t keys[NKEYS > 0 ? NKEYS : 1];
     uint32_t own_bitmap[NKEYS > 0 ? 1 : kBitmapWords];
     __device__ uint32_t* bitmap() { return NKEYS > 0 ? reinterpret_cast<uint32_t*>(keys) : own_bitmap; }
 };
 
+// A block barrier that orders LDS accesses only: unlike __syncthreads it does
+// not wait for the block's outstanding global stores, so a selection can run
+// while the scores the block just stored drain to memory.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int NT, class SH>
 __device__ uint64_t block_min_u64(uint64_t v, SH& sh) {
     v = vz::wave_min_u64(v);
     const int w = threadIdx.x / vz::kWave;
-    __syncthreads();
+    lds_barrier();
     if ((threadIdx.x % vz::kWave) == 0) sh.red64[w] = v;
-    __syncthreads();
+    lds_barrier();
     uint64_t r = sh.red64[0];
     for (int i = 1; i < NT / vz::kWave; ++i) r = sh.red64[i] < r ? sh.red64[i] : r;
     return r;
@@ -242,12 +249,12 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh,
         thr = tau;
         shift = 0;
         if (LK && E == 1 && found == 1) {
-            __syncthreads();  // the pair the minimum's owner wrote
+            lds_barrier();  // the pair the minimum's owner wrote
         } else if (LK) {
             // Holes: evicted slots below the budget; movers: kept slots at or
             // above it; the k-th mover fills the k-th hole, both in slot order
             // (at most kSmallE of each, so one thread pairs them).
-            __syncthreads();
+            lds_barrier();
             if (tid == 0) {
                 int32_t* const holes = sh.holes;  // in LDS: indexed at run time without scratch memory
                 int nh = 0;
@@ -271,7 +278,7 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh,
                 }
                 sh.nm = nm;
             }
-            __syncthreads();
+            lds_barrier();
         }
     } else if (E > kSmallE) {
         uint64_t prefix = 0;
@@ -427,19 +434,31 @@ __device__ void select_body(const SelJob<typename vz::Elem<DT>::T>& job, SH& sh,
 
 
 // The fold of Eq. (6) for every slot of one layer, then (when `select`) the
-// selection above, by a block of NT threads.  The decode step left, per KV
-// head g, every key's sum over g's query heads of p_hj in S[g * row + j]; the
-// new score is A = gamma A + ((S_0 + S_1) + ...), in that order, with the zero
-// pad for the new slot len - 1 (whose position is next_pos - 1, written here).
-// Each new score is stored and turned into the slot's rank key at once (kept
-// in registers for the first minimum round, in LDS when E >= 2), so the
-// selection starts without re-reading the scores.  With at most kSmallE
-// evictions the movers are among the E slots at or past the budget: their
-// K/V rows are loaded beside the fold's loads and their new score and
+// selection above, by the block of NT threads that finishes a layer's decode
+// step.  The decode left, per KV head g, every key's sum over g's query heads
+// of p_hj in S[g * row + j] (written by other workgroups of the running
+// kernel with device-coherent stores, so read here with device-coherent
+// loads); the new score is A = gamma A + ((S_0 + S_1) + ...), in that order,
+// with the zero pad for the new slot len - 1, whose position next_pos - 1 is
+// written here.  Each new score is stored and turned into the slot's rank key
+// at once (kept in registers for the first minimum round, in LDS when E >= 2),
+// so the selection starts without re-reading the scores.
+//
+// Two slot layouts: the sums are read as 16-byte vectors, four consecutive
+// slots per thread (4 (tid + r NT) + i), added up and handed over through LDS
+// to the layout of everything else, one slot per thread and round (tid + b NT),
+// which keeps the old scores' and positions' 4-byte accesses coalesced (those
+// rows have no 16-byte alignment).  The old scores and positions are loaded
+// (fold_prefetch) before the block knows it finishes the layer, so only the
+// sums' round trip follows the arrival.  Buffer descriptors bound every
+// access: slots past the old ones read as 0 (the zero pad) and stores past
+// len are dropped, with no index clamping or branches.
+//
+// With at most kSmallE evictions the movers are among the E slots at or past
+// the budget: their K/V rows are loaded at the start and their new score and
 // position kept in LDS, so that the moves after the selection are stores
-// only; the new slot's rows are taken from k_new / v_new.
-// COHERENT: the sums were written by other workgroups of the running kernel
-// (device-coherent stores), so they are read with device-coherent loads.
+// only.  The new slot's K/V rows are always taken from k_new / v_new (its
+// cache rows were written by other workgroups of the running kernel).
 template <class T>
 struct FoldLayer {
     float* A;
@@ -458,8 +477,35 @@ struct FoldLayer {
     bool select;         // false: the fold alone
 };
 
-template <int NT, int RB, int DT, int D, int NW, bool COHERENT, class SH>
-__device__ void fold_select_layer(const FoldLayer<typename vz::Elem<DT>::T>& f, SH& sh) {
+// The old scores and positions of a thread's slots tid + b NT, b < B.
+template <int B>
+struct FoldOld {
+    float a[B];
+    int32_t p[B];
+};
+
+constexpr int kBufferDword3 = 0x00020000;  // raw buffer descriptor word 3 (32-bit data format)
+constexpr int kCoherent = 16;              // buffer access cache policy: device scope (sc1)
+
+// Issues the loads of the old scores A and positions P of a layer of len
+// slots after the append (the new slot and those past it read as 0).
+template <int NT, int B>
+__device__ __forceinline__ void fold_prefetch(float* A, int32_t* P, int len, FoldOld<B>& o) {
+    const int tid = threadIdx.x;
+    const int old = len - 1;  // slots holding a previous score and position
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(A, 0, old * 4, kBufferDword3);
+    const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(P, 0, old * 4, kBufferDword3);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+        o.a[b] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ra, (tid + b * NT) * 4, 0, 0));
+        o.p[b] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(rp, (tid + b * NT) * 4, 0, 0));
+    }
+}
+
+// s_acc: LDS scratch of at least 4 R NT + 2 NT floats.  B NT and 4 R NT cover len.
+template <int NT, int B, int R, int DT, int D, int NW, class SH>
+__device__ void fold_select_layer(const FoldLayer<typename vz::Elem<DT>::T>& f, const FoldOld<B>& o, float* s_acc,
+                                  SH& sh) {
     using T = typename vz::Elem<DT>::T;
     constexpr int PER = vz::Elem<DT>::kPer16B;
     constexpr int CH = D / PER;
@@ -467,7 +513,6 @@ __device__ void fold_select_layer(const FoldLayer<typename vz::Elem<DT>::T>& f, 
     const int tid = threadIdx.x;
     float* const A = f.A;
     int32_t* const P = f.P;
-    const float* const S = f.S;
     const int len = f.len;
     const int32_t new_pos = f.next_pos - 1;
     const int32_t recent_from = f.next_pos - f.M;
@@ -497,62 +542,80 @@ __device__ void fold_select_layer(const FoldLayer<typename vz::Elem<DT>::T>& f, 
             piece_slot[i] = slot;
         }
     }
-    auto load_sum = [&](const float* p) -> float {
-        if constexpr (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        else return *p;
-    };
-    // the keys go to LDS only for the later minimum rounds (E >= 2) and the
-    // radix select; the first round takes each thread's smallest key
-    const bool keys_to_lds = E >= 2;
-    uint64_t my_best = ~0ull;
-    int my_best_j = -1;
-    // slots tid + (b0 + b) NT, b < B: every load issued before any use; indexes clamped
-    auto fold_round = [&](auto per_thread, int b0) {
-        constexpr int B = decltype(per_thread)::value;
-        int32_t pv[B];
-        float av[B], sv[B][NW];
+    // ---- the sums over the KV heads, in head order, four slots per thread ----
+    {
+        float4 acc[R];
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int j = min(tid + (b0 + b) * NT, len - 1);
-            pv[b] = P[j];
-            av[b] = A[j];
+        for (int g0 = 0; g0 < NW; g0 += 4) {  // at most 4 KV heads' loads in flight
+            constexpr int GB = NW < 4 ? NW : 4;
+            float4 v[GB][R];
 #pragma unroll
-            for (int g = 0; g < NW; ++g) sv[b][g] = load_sum(S + g * f.row + j);
+            for (int gg = 0; gg < GB; ++gg) {
+                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float*>(f.S + (g0 + gg) * f.row), 0, static_cast<int>(f.row) * 4, kBufferDword3);
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    v[gg][r] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                              rs, (tid + r * NT) * 16, 0, kCoherent));
+            }
+#pragma unroll
+            for (int gg = 0; gg < GB; ++gg)
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    if (g0 + gg == 0) {
+                        acc[r] = v[gg][r];
+                    } else {
+                        acc[r].x += v[gg][r].x;
+                        acc[r].y += v[gg][r].y;
+                        acc[r].z += v[gg][r].z;
+                        acc[r].w += v[gg][r].w;
+                    }
+                }
         }
 #pragma unroll
-        for (int b = 0; b < B; ++b) {
-            const int j = tid + (b0 + b) * NT;
-            if (j < len) {
-                float acc = sv[b][0];
+        for (int r = 0; r < R; ++r) *reinterpret_cast<float4*>(s_acc + 4 * (tid + r * NT)) = acc[r];
+    }
+    lds_barrier();
+    // ---- Eq. (6) and the rank keys, one slot per thread and round ----
+    // Branch-free: the keys go to LDS for every slot index the rounds cover
+    // (kNoKey past len) when the selection needs them there (E >= 2; the
+    // first minimum round takes each thread's smallest key from registers),
+    // and the rounds that can hold slots at or past the budget (the movers
+    // when E <= kSmallE) leave every new score in s_acc and every position in
+    // s_pos, whole rounds at a time.
+    static_assert(SH::kKeys >= B * NT, "a key for every slot index of the rounds");
+    const bool keys_to_lds = E >= 2;
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(A, 0, len * 4, kBufferDword3);
+    const int b_mov = pre ? f.budget / NT : B;  // first round holding a mover
+    int32_t* const s_pos = reinterpret_cast<int32_t*>(s_acc + 4 * R * NT);  // [2 NT]: rounds b_mov, b_mov + 1
+    uint64_t my_best = ~0ull;
+    int my_best_j = -1;
+    auto rounds = [&](auto keys) {
+        constexpr bool KEYS = decltype(keys)::value;
 #pragma unroll
-                for (int g = 1; g < NW; ++g) acc += sv[b][g];
-                const bool fresh = j == len - 1;
-                const float a_new = fmaf(f.gamma, fresh ? 0.f : av[b], acc);
-                A[j] = a_new;
-                const int32_t p = fresh ? new_pos : pv[b];
-                if (fresh) P[j] = p;
-                const uint64_t key = p >= f.n_sink && p < recent_from ? vz::rank_key(a_new, p) : kNoKey;
-                if (keys_to_lds) sh.keys[j] = key;
-                if (key < my_best) {  // kNoKey never wins: keys hold the position, so they are below ~0
-                    my_best = key;
-                    my_best_j = j;
-                }
-                if (pre && j >= f.budget) {
-                    sh.pre_a[j - f.budget] = a_new;
-                    sh.pre_p[j - f.budget] = p;
-                }
+        for (int b = 0; b < B; ++b) {
+            const int j = tid + b * NT;
+            const float a_new = fmaf(f.gamma, o.a[b], s_acc[j]);  // o.a is 0 for the new slot (zero pad)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, a_new), ra, j * 4, 0, 0);  // dropped past len
+            const int32_t p = j == len - 1 ? new_pos : o.p[b];
+            const bool mid = j < len && p >= f.n_sink && p < recent_from;
+            const uint64_t key = mid ? vz::rank_key(a_new, p) : kNoKey;
+            const bool better = key < my_best;  // kNoKey never wins: keys hold the position, so they are below ~0
+            my_best = better ? key : my_best;
+            my_best_j = better ? j : my_best_j;
+            if constexpr (KEYS) sh.keys[j] = key;
+            if (b == b_mov || b == b_mov + 1) {  // wave-uniform
+                s_acc[j] = a_new;
+                s_pos[j - b_mov * NT] = p;
             }
         }
     };
-    // slots per thread: RB - 1 or RB in one round while they suffice, else
-    // rounds of RB
-    const int spt = (len + NT - 1) / NT;
-    if (spt <= RB - 1) {
-        fold_round(std::integral_constant<int, RB - 1>{}, 0);
-    } else {
-        for (int b0 = 0; b0 < spt; b0 += RB) fold_round(std::integral_constant<int, RB>{}, b0);
-    }
-    __syncthreads();  // keys in LDS; new scores and the new position visible to the block
+    if (keys_to_lds)
+        rounds(std::true_type{});
+    else
+        rounds(std::false_type{});
+    if (tid == (len - 1) % NT) P[len - 1] = new_pos;  // Eq. (1): the new slot's position
+    lds_barrier();  // keys and movers in LDS (the scores' stores may still drain)
     if (!f.select || (E == 0 && f.kept == nullptr)) return;
     SelJob<T> job;
     job.A = A;
@@ -574,14 +637,12 @@ __device__ void fold_select_layer(const FoldLayer<typename vz::Elem<DT>::T>& f, 
     job.first_best = my_best;
     job.first_best_j = my_best_j;
     // The moves, always done here: the new slot's K/V rows come from k_new /
-    // v_new (its cache rows were written by other workgroups of a running
-    // kernel), its score and position from this block's own stores.
+    // v_new, its score and position from this block's own stores.
     auto move_rows = [&](int n_moves, const int32_t* src, const int32_t* dst) -> bool {
-        if (pre) {  // from the prefetched rows (pairs in LDS, at most kSmallE)
+        if (pre) {  // from LDS and the prefetched rows (at most kSmallE)
             if (tid < n_moves) {
-                const int sj = src[tid] - f.budget;
-                A[dst[tid]] = sh.pre_a[sj];
-                P[dst[tid]] = sh.pre_p[sj];
+                A[dst[tid]] = s_acc[src[tid]];
+                P[dst[tid]] = s_pos[src[tid] - b_mov * NT];
             }
 #pragma unroll
             for (int i = 0; i < NPIECE; ++i)
@@ -591,6 +652,7 @@ __device__ void fold_select_layer(const FoldLayer<typename vz::Elem<DT>::T>& f, 
                             *reinterpret_cast<uint4*>(piece_base[i] + static_cast<size_t>(dst[r]) * D) = piece[i];
             return true;
         }
+        __syncthreads();  // every new score and the new position stored (read back below)
         for (int r = tid; r < n_moves; r += NT) {
             A[dst[r]] = A[src[r]];
             P[dst[r]] = P[src[r]];
