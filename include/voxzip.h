@@ -219,6 +219,37 @@ VZ_API int voxzip_decode_evict(const void *q, const void *k_new, const void *v_n
                                size_t ws_bytes, void *stream);
 
 /*
+ * The generation step of voxzip_decode_evict for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same arguments except the workspace,
+ * the same launches and results, bit for bit.  Instead of a workspace it uses
+ * a scratch array of VZ_NOALLOC_SCRATCH_BYTES that the library holds on each
+ * GPU it runs on, from the first call on that GPU until the process ends.  It
+ * allocates nothing and calls no allocating routine.
+ *
+ *  The call runs on the current device; `stream` must belong to it.
+ *  Every call on one GPU shares that GPU's scratch array: calls that may
+ *  overlap on one GPU (concurrent streams, threads) race and must be
+ *  serialised by the caller.  The array needs no initialisation and may hold
+ *  any earlier call's contents.
+ *  Limit: calls whose workspace (voxzip_workspace_bytes(VZ_OP_DECODE_EVICT,
+ *  ...)) exceeds VZ_NOALLOC_SCRATCH_BYTES return VZ_ERR_WORKSPACE with the
+ *  sizes in voxzip_last_error() and queue nothing; the 48-layer, 4-KV-head,
+ *  d = 128 cache of 8194 slots needs 52.5 MB.
+ * Errors: those of voxzip_decode_evict, and VZ_ERR_HIP when the scratch
+ * array's device address cannot be found.
+ */
+#define VZ_NOALLOC_SCRATCH_BYTES (64u << 20)
+VZ_API int voxzip_decode_evict_noalloc(const void *q, const void *k_new, const void *v_new,
+                                       void *k_cache, void *v_cache, float *score, int32_t *pos,
+                                       void *out, int32_t len, int32_t next_pos, float gamma,
+                                       float sm_scale, int32_t budget, int32_t n_sink,
+                                       int32_t n_recent, int32_t *kept_pos_out,
+                                       int32_t *new_len_out, int32_t n_layers, int32_t n_q_heads,
+                                       int32_t kv_heads, int32_t d, int32_t cap, int32_t dtype,
+                                       void *stream);
+
+/*
  * Workspace bytes an operation needs for the given sizes (0 on a bad op).
  * n_q_heads is ignored for VZ_OP_EVICT.
  */

@@ -18,6 +18,7 @@ VZ_OK, VZ_ERR_INVALID, VZ_ERR_SHAPE, VZ_ERR_CAPACITY = 0, -1, -2, -3
 VZ_ERR_UNSUPPORTED, VZ_ERR_HIP, VZ_ERR_WORKSPACE = -4, -5, -6
 VZ_F32, VZ_BF16 = 0, 1
 VZ_OP_DECODE, VZ_OP_EVICT, VZ_OP_DECODE_EVICT = 1, 2, 3
+VZ_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _lib = None
 
@@ -45,6 +46,8 @@ def lib() -> ctypes.CDLL:
                                        i32, i32, i32, i32, i32, P, sz, P]
     L.voxzip_decode_evict.argtypes = [P, P, P, P, P, P, P, P, i32, i32, f32, f32, i32, i32, i32, P, P,
                                       i32, i32, i32, i32, i32, i32, P, sz, P]
+    L.voxzip_decode_evict_noalloc.argtypes = [P, P, P, P, P, P, P, P, i32, i32, f32, f32, i32, i32, i32, P, P,
+                                              i32, i32, i32, i32, i32, i32, P]
     L.voxzip_build_span_offsets.argtypes = [P, P, P, P, i32, ctypes.c_int64, i32, f32, P, P]
     L.voxzip_build_span_offsets.restype = ctypes.c_int
     L.voxzip_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
@@ -224,6 +227,32 @@ def voxzip_decode_evict(q, k_new, v_new, k_cache, v_cache, score, pos, out, leng
                                      float(sm_scale), int(budget), int(n_sink), int(n_recent), _ptr(kept_pos_out),
                                      ctypes.byref(new_len), L, Hq, Hkv, d, cap, _dtype_code(k_cache),
                                      _ptr(workspace), ws_bytes, _stream(stream)))
+    return int(new_len.value)
+
+
+def voxzip_decode_evict_noalloc(q, k_new, v_new, k_cache, v_cache, score, pos, out, length, next_pos, gamma,
+                                budget, n_sink=4, n_recent=-1, kept_pos_out=None, sm_scale=0.0,
+                                stream=None) -> int:
+    """voxzip_decode_evict without a workspace (the library's own per-GPU
+    scratch array); returns the new resident length."""
+    import torch
+    L, Hkv, cap, d = k_cache.shape
+    Hq = q.shape[1]
+    dt = k_cache.dtype
+    _expect(q, (L, Hq, d), "q", dt)
+    _expect(out, (L, Hq, d), "out", dt)
+    _expect(k_new, (L, Hkv, d), "k_new", dt)
+    _expect(v_new, (L, Hkv, d), "v_new", dt)
+    _expect(v_cache, k_cache.shape, "v_cache", dt)
+    _expect(score, (L, cap), "score", torch.float32)
+    _expect(pos, (L, cap), "pos", torch.int32)
+    _expect(kept_pos_out, (L, int(budget)), "kept_pos_out", torch.int32)
+    new_len = ctypes.c_int32(0)
+    _check(lib().voxzip_decode_evict_noalloc(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+                                             _ptr(score), _ptr(pos), _ptr(out), int(length), int(next_pos),
+                                             float(gamma), float(sm_scale), int(budget), int(n_sink), int(n_recent),
+                                             _ptr(kept_pos_out), ctypes.byref(new_len), L, Hq, Hkv, d, cap,
+                                             _dtype_code(k_cache), _stream(stream)))
     return int(new_len.value)
 
 

@@ -5,9 +5,16 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "vz_internal.h"
+
+// Scratch memory of voxzip_decode_evict_noalloc: one array per GPU, held
+// until the process ends.  In host code `scratch` names a host-side stand-in,
+// not device memory: only the address hipGetSymbolAddress returns for the
+// current device is ever used.
+static __device__ __align__(256) uint8_t scratch[VZ_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -254,25 +261,37 @@ int voxzip_evict_compact(void* k_cache, void* v_cache, float* score, int32_t* po
     return e == hipSuccess ? VZ_OK : hip_fail(fn, e);
 }
 
-int voxzip_decode_evict(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
-                        float* score, int32_t* pos, void* out, int32_t len, int32_t next_pos, float gamma,
-                        float sm_scale, int32_t budget, int32_t n_sink, int32_t n_recent, int32_t* kept_pos_out,
-                        int32_t* new_len_out, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
-                        int32_t cap, int32_t dtype, void* workspace, size_t ws_bytes, void* stream) {
-    static const char* fn = "voxzip_decode_evict";
+}  // extern "C"
+
+namespace {
+
+// Host checks of a generation step (both entry points); M receives the recent
+// window and need the workspace bytes.
+int check_step(const char* fn, const void* q, const void* k_new, const void* v_new, const void* k_cache,
+               const void* v_cache, const float* score, const int32_t* pos, const void* out, int32_t len,
+               int32_t next_pos, float gamma, float sm_scale, int32_t budget, int32_t n_sink, int32_t n_recent,
+               const int32_t* kept_pos_out, const int32_t* new_len_out, int32_t n_layers, int32_t n_q_heads,
+               int32_t kv_heads, int32_t d, int32_t cap, int32_t dtype, int32_t& M, size_t& need) {
     int rc = check_decode(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
                           n_layers, n_q_heads, kv_heads, d, cap, dtype);
     if (rc) return rc;
     if (!new_len_out) return fail(VZ_ERR_INVALID, fn, "null pointer");
     // the eviction sees the cache after the append
-    const int32_t T = len + 1;
     if (next_pos == INT32_MAX) return fail(VZ_ERR_INVALID, fn, "next_pos + 1 overflows");
-    int32_t M = 0;
-    rc = check_evict(fn, T, budget, n_sink, n_recent, next_pos + 1, kept_pos_out, cap, M);
+    rc = check_evict(fn, len + 1, budget, n_sink, n_recent, next_pos + 1, kept_pos_out, cap, M);
     if (rc) return rc;
+    need = decode_evict_split(n_layers, n_q_heads, kv_heads, d, cap) + vz_evict_ws_bytes(n_layers, cap, 0);
+    return VZ_OK;
+}
+
+// The generation step's launches, arguments checked (workspace of ws_bytes >= need).
+int launch_step(const char* fn, const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                float* score, int32_t* pos, void* out, int32_t len, int32_t next_pos, float gamma, float sm_scale,
+                int32_t budget, int32_t n_sink, int32_t M, int32_t* kept_pos_out, int32_t* new_len_out,
+                int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d, int32_t cap, int32_t dtype,
+                void* workspace, size_t ws_bytes, void* stream) {
+    const int32_t T = len + 1;
     const size_t split = decode_evict_split(n_layers, n_q_heads, kv_heads, d, cap);
-    const size_t need = split + vz_evict_ws_bytes(n_layers, cap, 0);
-    if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
     hipStream_t st = static_cast<hipStream_t>(stream);
     VzDecodeArgs da{q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale,
                     n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace, split, VzRagged{},
@@ -298,6 +317,77 @@ int voxzip_decode_evict(const void* q, const void* k_new, const void* v_new, voi
     if (e != hipSuccess) return hip_fail(fn, e);
     *new_len_out = T < budget ? T : budget;
     return VZ_OK;
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (each GPU holds its own copy of the array).
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];
+
+int scratch_address(const char* fn, void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(fn, e);
+    if (dev < 0 || dev >= kMaxDevices) return fail(VZ_ERR_UNSUPPORTED, fn, "device index beyond 63");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_dev[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(fn, e);
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return VZ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int voxzip_decode_evict(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                        float* score, int32_t* pos, void* out, int32_t len, int32_t next_pos, float gamma,
+                        float sm_scale, int32_t budget, int32_t n_sink, int32_t n_recent, int32_t* kept_pos_out,
+                        int32_t* new_len_out, int32_t n_layers, int32_t n_q_heads, int32_t kv_heads, int32_t d,
+                        int32_t cap, int32_t dtype, void* workspace, size_t ws_bytes, void* stream) {
+    static const char* fn = "voxzip_decode_evict";
+    int32_t M = 0;
+    size_t need = 0;
+    int rc = check_step(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale, budget,
+                        n_sink, n_recent, kept_pos_out, new_len_out, n_layers, n_q_heads, kv_heads, d, cap, dtype, M,
+                        need);
+    if (rc) return rc;
+    if (!ws_ok(workspace, ws_bytes, need)) return fail(VZ_ERR_WORKSPACE, fn, "workspace missing, misaligned or too small");
+    return launch_step(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale, budget,
+                       n_sink, M, kept_pos_out, new_len_out, n_layers, n_q_heads, kv_heads, d, cap, dtype, workspace,
+                       ws_bytes, stream);
+}
+
+int voxzip_decode_evict_noalloc(const void* q, const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                                float* score, int32_t* pos, void* out, int32_t len, int32_t next_pos, float gamma,
+                                float sm_scale, int32_t budget, int32_t n_sink, int32_t n_recent,
+                                int32_t* kept_pos_out, int32_t* new_len_out, int32_t n_layers, int32_t n_q_heads,
+                                int32_t kv_heads, int32_t d, int32_t cap, int32_t dtype, void* stream) {
+    static const char* fn = "voxzip_decode_evict_noalloc";
+    int32_t M = 0;
+    size_t need = 0;
+    int rc = check_step(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale, budget,
+                        n_sink, n_recent, kept_pos_out, new_len_out, n_layers, n_q_heads, kv_heads, d, cap, dtype, M,
+                        need);
+    if (rc) return rc;
+    if (need > VZ_NOALLOC_SCRATCH_BYTES) {
+        g_last_error = std::string(fn) + ": the call needs " + std::to_string(need) +
+                       " bytes of scratch memory (voxzip_workspace_bytes(VZ_OP_DECODE_EVICT, ...)); this entry point "
+                       "holds " + std::to_string(static_cast<size_t>(VZ_NOALLOC_SCRATCH_BYTES)) +
+                       ": use voxzip_decode_evict with a workspace";
+        return VZ_ERR_WORKSPACE;
+    }
+    void* ws = nullptr;
+    rc = scratch_address(fn, &ws);
+    if (rc) return rc;
+    return launch_step(fn, q, k_new, v_new, k_cache, v_cache, score, pos, out, len, next_pos, gamma, sm_scale, budget,
+                       n_sink, M, kept_pos_out, new_len_out, n_layers, n_q_heads, kv_heads, d, cap, dtype, ws,
+                       VZ_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int voxzip_fuse_spans_ragged(const void* k_in, const void* v_in, const int64_t* in_base, const int32_t* T_in,
