@@ -45,6 +45,7 @@ extern "C" {
 #define VZ_ERR_UNSUPPORTED -4 /* dtype / head size / group size this build does not serve */
 #define VZ_ERR_HIP -5         /* a HIP call failed; voxzip_last_error() has its text */
 #define VZ_ERR_WORKSPACE -6   /* workspace missing, not 16-byte aligned, or smaller than voxzip_workspace_bytes() */
+#define VZ_IDLE 1             /* per-sequence status of a ragged call: an idle batch slot (cap[s] == 0), skipped */
 
 /* Element types. */
 #define VZ_F32 0
@@ -273,10 +274,17 @@ VZ_API size_t voxzip_workspace_bytes(int32_t op, int32_t n_layers, int32_t n_q_h
  *  Per-sequence values (seq_base int64, cap / len / budget / next_pos int32,
  *  [n_seqs] each) are DEVICE arrays, read by the kernels: host code never
  *  waits for them, so a whole serving loop can stay on the device.
+ *  Idle batch slots: a sequence with cap[s] == 0 is an idle slot of the
+ *  batch (no request holds it): every ragged call skips it without reading
+ *  or writing anything of it and reports VZ_IDLE.  A serving loop retires a
+ *  finished request by setting its cap to 0 and admits a new one into the
+ *  slot by restoring the cap and fusing the request's prefill there, with no
+ *  change to the launch shapes (a captured HIP graph of the step stays valid).
  *  status: NULL or int32 [n_seqs], device: receives VZ_OK per served
- *  sequence, or the error code of a sequence whose values are out of range;
- *  such a sequence is skipped (nothing of it is read or written, its outputs
- *  keep their previous contents).  Host-side errors are returned as usual.
+ *  sequence, VZ_IDLE per idle slot, or the error code of a sequence whose
+ *  values are out of range; such a sequence is skipped (nothing of it is
+ *  read or written, its outputs keep their previous contents).  Host-side
+ *  errors are returned as usual.
  *
  * Workspace bytes of a ragged call (0 on a bad op or sizes out of range).
  */

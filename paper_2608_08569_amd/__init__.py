@@ -16,6 +16,7 @@ LIB_PATH = os.environ.get("VOXZIP_LIB", os.path.join(HERE, "libvoxzip.so"))
 
 VZ_OK, VZ_ERR_INVALID, VZ_ERR_SHAPE, VZ_ERR_CAPACITY = 0, -1, -2, -3
 VZ_ERR_UNSUPPORTED, VZ_ERR_HIP, VZ_ERR_WORKSPACE = -4, -5, -6
+VZ_IDLE = 1  # per-sequence status of a ragged call: an idle batch slot (cap 0)
 VZ_F32, VZ_BF16 = 0, 1
 VZ_OP_DECODE, VZ_OP_EVICT, VZ_OP_DECODE_EVICT = 1, 2, 3
 VZ_NOALLOC_SCRATCH_BYTES = 64 << 20

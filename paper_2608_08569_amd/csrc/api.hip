@@ -144,6 +144,7 @@ const char* voxzip_status_string(int status) {
         case VZ_ERR_UNSUPPORTED: return "unsupported configuration";
         case VZ_ERR_HIP: return "HIP error";
         case VZ_ERR_WORKSPACE: return "workspace too small";
+        case VZ_IDLE: return "idle batch slot";
         default: return "unknown status";
     }
 }

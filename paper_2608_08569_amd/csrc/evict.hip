@@ -51,10 +51,12 @@ __global__ __launch_bounds__(kSel) void select_kernel(const VzEvictArgs a, int32
     select_body<kSel, DT, D, LK>(job, sh);
 }
 
-// Status of sequence s for an eviction (VZ_OK when it can be served).
+// Status of sequence s for an eviction (VZ_OK when it can be served, VZ_IDLE
+// for an idle slot).
 __device__ int ragged_evict_status(const VzRagged& r, int s, int n_sink, int n_recent, bool kept) {
     const int64_t b = r.base[s];
     const int c = r.cap[s], n = r.len[s], B = r.budget[s], p = r.next_pos[s];
+    if (c == 0) return VZ_IDLE;
     if (n < 0 || c < 1 || b < 0 || b > r.total - c) return VZ_ERR_INVALID;
     if (n > c) return VZ_ERR_CAPACITY;
     const int M = n_recent < 0 ? B / 5 : n_recent;

@@ -47,10 +47,12 @@ struct FuseArgs {
     int32_t max_spans;
 };
 
-// Status of sequence s of a ragged fusion (VZ_OK when it can be served).
+// Status of sequence s of a ragged fusion (VZ_OK when it can be served,
+// VZ_IDLE for an idle slot).
 __device__ int ragged_fuse_status(const FuseArgs& a, int s) {
     const int64_t ib = a.in_base[s], ob = a.off_base[s], b = a.base[s];
     const int T = a.T_in_s[s], n = a.n_spans_s[s], c = a.cap[s];
+    if (c == 0) return VZ_IDLE;
     if (T < 0 || n < 0 || c < 1 || ib < 0 || ib > a.in_plane - T || ob < 0 || ob > a.total_off - n - 1 || b < 0 ||
         b > a.out_plane - c)
         return VZ_ERR_INVALID;

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported():
 def test_status_strings_and_version():
     L = vz.lib()
     assert L.voxzip_version() >= 100
-    for code in (0, -1, -2, -3, -4, -5, -6):
+    for code in (0, -1, -2, -3, -4, -5, -6, vz.VZ_IDLE):
         assert L.voxzip_status_string(code).decode() not in ("", "unknown status")
 
 

@@ -151,12 +151,13 @@ def test_ragged_decode_one_sequence_and_gamma_edges():
 
 
 def test_ragged_decode_skips_invalid_sequences():
-    """Sequences 1-5 carry out-of-range values; they are reported and nothing of
-    them is touched, while sequence 0 is served normally."""
+    """Sequences 1-5 carry out-of-range values and sequence 6 is an idle slot
+    (capacity 0); they are reported and nothing of them is touched, while
+    sequence 0 is served normally."""
     t = torch()
     import paper_2608_08569_amd as vz
     L, Hq, Hkv, d, dtype = 2, 32, 4, 128, synth.DT_BF16
-    lens = np.array([100, 200, 50, 300, 40, 60], dtype=np.int64)
+    lens = np.array([100, 200, 50, 300, 40, 60, 80], dtype=np.int64)
     next_pos = lens + 1
     caps = lens + 8
     pk = Packed(caps, gap=4, seed=5)
@@ -169,8 +170,9 @@ def test_ragged_decode_skips_invalid_sequences():
     next_d[3] = -1                       # negative position
     len_d[4] = 2 ** 31 - 1               # len + 1 would overflow
     len_d[5] = -1
+    cap_d[6] = 0                         # an idle batch slot
     expect = [vz.VZ_OK, vz.VZ_ERR_CAPACITY, vz.VZ_ERR_INVALID, vz.VZ_ERR_INVALID, vz.VZ_ERR_CAPACITY,
-              vz.VZ_ERR_INVALID]
+              vz.VZ_ERR_INVALID, vz.VZ_IDLE]
     n = len(lens)
     key = synth.stream_key(5, "ragged-invalid")
     q = _storage_noise(key, (n, L, Hq, d), dtype)
@@ -273,29 +275,30 @@ def test_ragged_evict_skips_invalid_sequences():
     t = torch()
     import paper_2608_08569_amd as vz
     L, Hkv, d, dtype = 2, 4, 128, synth.DT_BF16
-    lens = np.array([300, 300, 300, 300, 300], dtype=np.int64)
+    lens = np.array([300, 300, 300, 300, 300, 300], dtype=np.int64)
     next_pos = lens + 10
     pk = Packed(lens + 2, gap=2, seed=9)
     K, V, S, P = _packed_state(pk, L, Hkv, d, dtype, lens, next_pos, 9)
     Kd, Vd, Sd, Pd = to_dev(K), to_dev(V), to_dev(S), to_dev(P)
     base_d, cap_d = pk.dev()
-    budget = _i32([200, 0, 200, 200, 200])     # seq 1: budget < 1
+    budget = _i32([200, 0, 200, 200, 200, 200])  # seq 1: budget < 1
     len_d = _i32(lens)
     len_d[2] = 303                              # len > cap
     nxt = _i32(next_pos)
     nxt[3] = 100                                # next_pos < len
     base_d[4] = -1
-    status = _i32(np.full(5, -99))
-    new_len = _i32(np.full(5, -9))
-    ws = vz.workspace_ragged(vz.VZ_OP_EVICT, L, 8, Hkv, d, pk.total, 5)
+    cap_d[5] = 0                                # an idle batch slot
+    status = _i32(np.full(6, -99))
+    new_len = _i32(np.full(6, -9))
+    ws = vz.workspace_ragged(vz.VZ_OP_EVICT, L, 8, Hkv, d, pk.total, 6)
     vz.voxzip_evict_compact_ragged(Kd, Vd, Sd, Pd, base_d, cap_d, len_d, budget, nxt, new_len_out=new_len,
                                    status=status, workspace=ws)
     t.cuda.synchronize()
     assert from_dev(status).tolist() == [vz.VZ_OK, vz.VZ_ERR_INVALID, vz.VZ_ERR_CAPACITY, vz.VZ_ERR_INVALID,
-                                         vz.VZ_ERR_INVALID]
-    assert from_dev(new_len).tolist() == [200, 300, 303, 300, 300]
+                                         vz.VZ_ERR_INVALID, vz.VZ_IDLE]
+    assert from_dev(new_len).tolist() == [200, 300, 303, 300, 300, 300]
     K1, S1, P1 = from_dev(Kd), from_dev(Sd), from_dev(Pd)
-    for s in range(1, 5):
+    for s in range(1, 6):
         sl = pk.sl(s)
         assert np.array_equal(K1[:, :, sl], K[:, :, sl]) and np.array_equal(S1[:, sl], S[:, sl])
         assert np.array_equal(P1[:, sl], P[:, sl])

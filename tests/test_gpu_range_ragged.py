@@ -151,18 +151,18 @@ def test_ragged_range_gamma_edges():
 
 
 def test_ragged_range_skips_invalid_and_overflowing_sequences():
-    """A sequence with no free slot and one outside the planes are skipped
-    (status says why, nothing of theirs written); two sequences over the
+    """A sequence with no free slot, one outside the planes and an idle slot
+    are skipped (status says why, nothing of theirs written); two sequences over the
     same 20000 slots (3 parts each) need more parts than the table holds
     (2 sequences + 3 = 5): the first in the order (the smaller index, as the
     parts are alike) is served, the other reported."""
     t = torch()
     import paper_2608_08569_amd as vz
     L, Hq, Hkv = 32, 32, 4
-    # sequence 0: full (len = cap); 1: fine; 2: base past the planes
-    caps = np.array([50, 400, 60])
+    # sequence 0: full (len = cap); 1: fine; 2: base past the planes; 3: an idle slot (cap 0)
+    caps = np.array([50, 400, 60, 70])
     pk = Packed(caps, gap=2, seed=3)
-    lens = np.array([50, 399, 10])
+    lens = np.array([50, 399, 10, 20])
     next_pos = lens + 4
     K, V, S, P = _packed(pk, L, Hkv, np.minimum(lens, caps - 1), next_pos, 3)
     Kd, Vd, Sd, Pd = to_dev(K), to_dev(V), to_dev(S), to_dev(P)
@@ -170,18 +170,20 @@ def test_ragged_range_skips_invalid_and_overflowing_sequences():
     base[2] = pk.total - 5
     base_d = t.from_numpy(base).cuda()
     cap_d = t.from_numpy(pk.caps.copy()).cuda()
-    status = _i32(np.full(3, -99))
-    q, kn, vn = _inputs(3, 0, 3, L, Hq, Hkv)
-    out_d = t.zeros(3, L, Hq, D, dtype=t.bfloat16, device="cuda")
-    ws = vz.workspace_ragged(vz.VZ_OP_DECODE, L, Hq, Hkv, D, pk.total, 3)
+    cap_d[3] = 0
+    status = _i32(np.full(4, -99))
+    q, kn, vn = _inputs(3, 0, 4, L, Hq, Hkv)
+    out_d = t.zeros(4, L, Hq, D, dtype=t.bfloat16, device="cuda")
+    ws = vz.workspace_ragged(vz.VZ_OP_DECODE, L, Hq, Hkv, D, pk.total, 4)
     ws.fill_(0x55)
     vz.voxzip_decode_attend_score_ragged(to_dev(q), to_dev(kn), to_dev(vn), Kd, Vd, Sd, Pd, out_d, base_d, cap_d,
                                          _i32(lens), _i32(next_pos), 0.95, status=status, workspace=ws)
     t.cuda.synchronize()
     st = from_dev(status)
-    assert st[0] == vz.VZ_ERR_CAPACITY and st[1] == vz.VZ_OK and st[2] == vz.VZ_ERR_INVALID
+    assert st.tolist() == [vz.VZ_ERR_CAPACITY, vz.VZ_OK, vz.VZ_ERR_INVALID, vz.VZ_IDLE]
+    assert not from_dev(out_d)[3].any()
     K1, S1, P1 = from_dev(Kd), from_dev(Sd), from_dev(Pd)
-    for s in (0, 2):
+    for s in (0, 2, 3):
         sl = pk.sl(s)
         assert np.array_equal(K1[:, :, sl], K[:, :, sl]) and np.array_equal(S1[:, sl], S[:, sl])
         assert np.array_equal(P1[:, sl], P[:, sl])
