@@ -37,6 +37,7 @@ import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 PROFILE_PMC = os.path.join(ROOT, "profiles", "decode_long32k_pmc.md")
+PROFILE_KEPT = os.path.join(ROOT, "profiles", "kept_sets_long32k.md")
 KERNEL_SRC = [os.path.join(ROOT, "paper_2608_08569_amd", "csrc", f)
               for f in ("decode_range.hip", "decode_mfma.h", "select.h", "vz_internal.h")]
 
@@ -75,6 +76,23 @@ def read_traffic():
     if not (m_sha and m_b) or m_sha.group(1) != kernel_sha():
         return None
     return float(m_b.group(1))
+
+
+def read_kept_agreement():
+    """The free-running kept-set agreement with the oracle recorded by
+    ``bench.py --kept-sets`` (informational), only if it was taken on the
+    current kernel source."""
+    if not os.path.exists(PROFILE_KEPT):
+        return None
+    txt = open(PROFILE_KEPT).read()
+    f = {k: re.search(rf"{k}:\s*(\S+)", txt) for k in ("kernel_source_sha", "kept_jaccard_min", "kept_jaccard_mean",
+                                                       "kept_layers")}
+    if not all(f.values()) or f["kernel_source_sha"].group(1) != kernel_sha():
+        return None
+    return {"jaccard_min": float(f["kept_jaccard_min"].group(1)),
+            "jaccard_mean": float(f["kept_jaccard_mean"].group(1)),
+            "layers": [int(x) for x in f["kept_layers"].group(1).split(",")], "steps": 256,
+            "source": "profiles/kept_sets_long32k.md (bench.py --kept-sets: GPU and oracle free running)"}
 
 
 def cpu_model() -> str:
@@ -215,6 +233,64 @@ def cpu_baseline(w, n_layers_sample: int, max_seconds: float):
                    f"{n_layers_sample} of {w.n_layers} layers, after host-side fusion; time per step "
                    f"scaled by {w.n_layers}/{n_layers_sample} to a whole-model token; host CPU {cpu_model()}"),
     }
+
+
+def kept_sets_report(args, torch, vz) -> dict:
+    """Free-running agreement of the kept sets (Sec. 3.2.2 Eq. 9): the 32k
+    request (fusion, then 256 generation steps with eviction) on the GPU over
+    all layers, and the oracle's own run (fp64 scores) over a sample of the
+    layers from the same inputs, neither side ever resynchronised.  After
+    every step, per sampled layer, the Jaccard index of the two resident
+    position sets.  GPU and oracle scores differ by rounding (bfloat16
+    probabilities on the GPU), so a near-tie at the eviction threshold can
+    keep a different slot; the two runs then go on from different caches."""
+    import oracle
+    w = synth.workload("long32k")
+    L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.kv_heads, w.d
+    layers = [int(x) for x in args.kept_layers.split(",")]
+    off = synth.offsets_from_lengths(synth.span_lengths(w))
+    n = len(off) - 1
+    t0 = time.time()
+    k_in = synth.prefill_kv(w, "k")
+    v_in = synth.prefill_kv(w, "v")
+    to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    cap = max(n, w.budget) + 2
+    K = torch.zeros(L, Hkv, cap, d, dtype=torch.bfloat16, device="cuda")
+    V = torch.zeros_like(K)
+    S = torch.zeros(L, cap, dtype=torch.float32, device="cuda")
+    P = torch.zeros(L, cap, dtype=torch.int32, device="cuda")
+    out = torch.zeros(L, Hq, d, dtype=torch.bfloat16, device="cuda")
+    ws = vz.workspace(vz.VZ_OP_DECODE_EVICT, L, Hq, Hkv, d, cap)
+    vz.voxzip_fuse_spans(to_dev(k_in), to_dev(v_in), torch.from_numpy(off).cuda(), K, V, S, P)
+    idx = torch.tensor(layers, dtype=torch.long, device="cuda")
+    run = oracle.Run(k_in[layers], v_in[layers], off, w.dtype, Hq, cap, w.gamma, w.budget)
+    del k_in, v_in
+    log(f"[kept] inputs and fusion {time.time() - t0:.1f}s; oracle on layers {layers}")
+    length, nxt = n, n
+    jac = np.zeros((args.decode_steps, len(layers)))
+    for t in range(args.decode_steps):
+        q, kn, vn = synth.decode_inputs(w, t)
+        length = vz.voxzip_decode_evict(to_dev(q), to_dev(kn), to_dev(vn), K, V, S, P, out, length, nxt, w.gamma,
+                                        w.budget, workspace=ws)
+        nxt += 1
+        run.step(q[layers], kn[layers], vn[layers])
+        assert run.len == length
+        gpu_pos = P.index_select(0, idx)[:, :length].cpu().numpy()
+        for j in range(len(layers)):
+            a, b = set(gpu_pos[j].tolist()), set(run.pos[j, :length].tolist())
+            jac[t, j] = len(a & b) / len(a | b)
+        if t % 32 == 31:
+            log(f"[kept] step {t + 1}: mean Jaccard {jac[t].mean():.5f}")
+    diverged = [int(np.argmax(jac[:, j] < 1.0)) if np.any(jac[:, j] < 1.0) else None for j in range(len(layers))]
+    return {"kept_set_agreement": {
+        "workload": "long32k", "layers": layers, "steps": args.decode_steps, "budget": w.budget,
+        "jaccard_final": [float(x) for x in jac[-1]],
+        "jaccard_min": float(jac.min()),
+        "jaccard_mean": float(jac.mean()),
+        "first_step_with_a_difference": diverged,
+        "steps_identical_frac": float(np.mean(jac == 1.0)),
+        "curve_every_16_steps": [float(x) for x in jac.mean(axis=1)[15::16]],
+    }}
 
 
 class Sequence:
@@ -534,6 +610,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-report", action="store_true",
                     help="only time the CPU oracle per workload (single- and multi-threaded); no GPU work")
+    ap.add_argument("--kept-sets", action="store_true",
+                    help="only compare the GPU's free-running kept sets with the oracle's (long32k, sampled layers)")
+    ap.add_argument("--kept-layers", default="0,16,32,47", help="layers the oracle runs for --kept-sets")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--workload", default="long32k",
@@ -558,6 +637,10 @@ def main():
     vz.lib()  # fail loudly if the HIP library is not built
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
+
+    if args.kept_sets:
+        print(json.dumps(kept_sets_report(args, torch, vz)), flush=True)
+        return
 
     if args.copy_probe:
         n = 1 << 30
@@ -741,6 +824,9 @@ def main():
             },
         },
     }
+    kept = read_kept_agreement()
+    if kept is not None:
+        result["kept_set_agreement"] = kept
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_layers, args.cpu_seconds)
     print(json.dumps(result), flush=True)
