@@ -7,28 +7,25 @@
 // (layer, KV head) items and a short enough cache go to the whole-range path
 // (decode_range.hip) instead.
 //
-// Attend kernel: work item = (layer, key chunk of <= 128 keys).  A workgroup
-// has one wave per KV head; wave g streams K and V rows of head g over the
-// chunk.  Registers stay under 128 per lane so that four workgroups share a
-// CU.
-//   pass 1  S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (M = 16 keys, N = 16
+// Attend kernel: work item = (layer, key chunk of <= 128 keys, KV head), a
+// workgroup of four waves, one 32-key tile each (the K and V tiles of a wave
+// are requested at once: one memory round trip per chunk).
+//   logits  S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (M = 16 keys, N = 16
 //           query-head columns of which n_q/n_kv <= 8 are used, K = 32
 //           channels).  K tiles of 32 rows are loaded fully coalesced (4 whole
 //           rows per 1 KB instruction), stored to LDS with padded rows and
-//           read back with ds_read_b128 in the A-operand layout.  One tile is
-//           in flight while the previous one is multiplied; the first V tile
-//           follows the last K tile.  The logits of an odd 16-key tile are
-//           moved into the unused head columns 8..15 of the even tile's
-//           registers (DPP row rotate by 8), so 128 keys x 8 heads take 16
+//           read back with ds_read_b128 in the A-operand layout.  The logits
+//           of the odd 16-key half of a tile are moved into the unused head
+//           columns 8..15 (DPP row rotate by 8), so 32 keys x 8 heads take 4
 //           registers per lane.
-//   stats   chunk-local max m_c and sum l_c of exp2 per head; the registers
-//           then hold p~ = exp2(s - m_c).  (m_c, l_c) and p~ (bfloat16,
-//           64 bytes per key over the 32 heads of the workload) go to the
-//           workspace.
-//   pass 2  O_c = P V: V tiles take the same coalesced path into LDS and are
-//           read back with ds_read_b64_tr_b16 directly in the B-operand
-//           layout; P is rebuilt from the packed p~ registers with one row
-//           rotate.  O_c (relative to m_c) goes to the workspace in bfloat16.
+//   stats   the chunk's max m_c per head (the four waves' maxima through
+//           LDS); p~ = exp2(s - m_c) and the sum l_c of exp2 per head.
+//           (m_c, l_c) and p~ (bfloat16) go to the workspace.
+//   P V     V tiles take the same coalesced path into LDS and are read back
+//           with ds_read_b64_tr_b16 directly in the B-operand layout; P is
+//           rebuilt from p~ with one row rotate.  The four waves' O (fp32)
+//           are summed in wave order through LDS; O_c (relative to m_c) goes
+//           to the workspace in bfloat16.
 // Output kernel: per (head, layer), the output row merged from the chunk
 // partials, and the layer's (max, sum) of the head.  Fold kernel: per (chunk,
 // layer), the chunk's scores A[j] = gamma A[j] + sum_h p_hj from p~ and one
@@ -44,8 +41,6 @@ namespace {
 
 using namespace vz_mfma;
 
-constexpr int ATTEND_WG_PER_CU = 4;  // resident attend workgroups per CU (128 VGPRs)
-constexpr int ATTEND_DEEP_MAX_ITEMS = 512;  // attend grids this small keep four tiles in flight per wave
 // Decode workspace header: 256 reserved bytes (a ragged call keeps its table
 // sizes there), then one arrival counter per layer (whole-range path, zero
 // after every call), padded to 256 bytes.
@@ -90,21 +85,54 @@ struct SeqItem {
     int64_t base;    // its first slot in the planes
 };
 
+// Flat chunk f of a ragged call, found by a whole wave: each lane loads one
+// sequence's values (64 sequences per round), a wave scan of their chunk
+// counts finds the owner of f, and the owner's values are forwarded from the
+// lane that loaded them, so the kernel waits for one round of loads.  False
+// when f lies past the call's chunks (or past the nc_max rows).
+__device__ __forceinline__ bool locate_ragged_chunk(const FusedArgs& a, int f, SeqItem& it, int& c) {
+    const VzRagged& r = a.rag;
+    const int lane = threadIdx.x % vz::kWave;
+    int run = 0;
+    for (int s0 = 0; s0 < r.n && run <= a.nc_max; s0 += vz::kWave) {
+        const int su = min(s0 + lane, r.n - 1);  // load for every lane, mask after
+        const int64_t b = r.base[su];
+        const int cp = r.cap[su], ln = r.len[su], np = r.next_pos[su];
+        const bool ok = s0 + lane < r.n && vz::decode_status_of(b, cp, ln, np, r.total) == VZ_OK;
+        const int n = ok ? (ln + CHUNK) / CHUNK : 0;
+        int incl = n;
+#pragma unroll
+        for (int o = 1; o < vz::kWave; o <<= 1) {
+            const int t = __shfl_up(incl, o, vz::kWave);
+            if (lane >= o) incl += t;
+        }
+        const unsigned long long hit = __ballot(run + incl > f);
+        if (hit) {
+            const int src = __builtin_ctzll(hit);
+            const int nc = __builtin_amdgcn_readfirstlane(__shfl(n, src, vz::kWave));
+            const int first = __builtin_amdgcn_readfirstlane(run + __shfl(incl, src, vz::kWave) - nc);
+            if (first + nc > a.nc_max) return false;
+            it.s = s0 + src;
+            it.len = __builtin_amdgcn_readfirstlane(__shfl(ln, src, vz::kWave));
+            it.next_pos = __builtin_amdgcn_readfirstlane(__shfl(np, src, vz::kWave));
+            const uint32_t lo = __builtin_amdgcn_readfirstlane(__shfl(static_cast<int>(b), src, vz::kWave));
+            const uint32_t hi = __builtin_amdgcn_readfirstlane(__shfl(static_cast<int>(b >> 32), src, vz::kWave));
+            it.base = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+            it.n_chunks = nc;
+            it.first = first;
+            c = f - first;
+            return true;
+        }
+        run += __builtin_amdgcn_readfirstlane(__shfl(incl, vz::kWave - 1, vz::kWave));
+    }
+    return false;
+}
+
 // Flat chunk f of a call: false when it holds no work.
 template <bool RAG>
 __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem& it, int& c) {
     if constexpr (RAG) {
-        int first = 0, nc = 0;
-        const int s = vz::ragged_locate(f, a.rag.n, a.nc_max, [&](int t) { return ragged_chunks(a.rag, t); },
-                                        first, nc);
-        if (s < 0 || first + nc > a.nc_max) return false;
-        it.s = s;
-        it.len = __builtin_amdgcn_readfirstlane(a.rag.len[s]);
-        it.next_pos = __builtin_amdgcn_readfirstlane(a.rag.next_pos[s]);
-        it.n_chunks = nc;
-        it.first = first;
-        it.base = a.rag.base[s];
-        c = f - first;
+        return locate_ragged_chunk(a, f, it, c);
     } else {
         if (f >= a.n_chunks) return false;
         it.s = 0;
@@ -118,60 +146,63 @@ __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem
     return true;
 }
 
-// DEPTH: K/V tiles in flight per wave.  1 keeps the registers within four
-// resident workgroups per CU; 4 (the K tiles at once, each V tile issued as
-// its K slot frees) shortens the chain of dependent loads for grids too small
-// to fill the GPU, where occupancy does not matter.  The arithmetic is the
-// same, so are the bits.
-template <int NW, bool RAG, int DEPTH>
-__global__ __launch_bounds__(64 * NW, DEPTH == 1 ? ATTEND_WG_PER_CU : 1) void decode_attend_kernel(const FusedArgs a) {
-    __shared__ __attribute__((aligned(16))) uint8_t s_tile[NW][TILE_BYTES];
+// Attend kernel: work item = (layer, chunk, KV head), a workgroup of SPLIT_W
+// waves in which wave w owns keys [VT w, VT w + VT) of the chunk.  Each wave
+// requests its K and V tile (16 KB) before anything else, so a chunk costs
+// one memory round trip, and a one-layer call over 8k keys spreads its 16 MB
+// over 260 workgroups.  The waves agree on the chunk's max per head through
+// LDS, then sum their exp2 sums and partial outputs in wave order; the
+// partial results of (chunk, query head) go to the workspace for the
+// finishing kernels.
+constexpr int SPLIT_W = CHUNK / VT;  // waves per chunk: one 32-key tile each
+template <int NW, bool RAG>
+__global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const FusedArgs a) {
+    constexpr int OS = D + 4;  // padded LDS row of a wave's partial output (floats)
+    static_assert(SPLIT_W * GMAX * OS * 4 <= SPLIT_W * TILE_BYTES, "the partial outputs fit in the tile buffers");
+    __shared__ __attribute__((aligned(16))) uint8_t s_tile[SPLIT_W][TILE_BYTES];
+    __shared__ __attribute__((aligned(16))) uint16_t s_p[GMAX][CHUNK];  // p~ of the chunk, per head
+    __shared__ float s_m[SPLIT_W][GMAX], s_l[SPLIT_W][GMAX];
     const int tid = threadIdx.x;
-    // wave-uniform values go through readfirstlane so that addresses built
-    // from them stay scalar (buffer descriptors in SGPRs)
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int q4 = lane >> 4, r16 = lane & 15;
-    const int hi = r16 >> 3;          // 0: even tile of a pair, 1: odd tile (packed lanes)
-    const int hh = r16 & 7;           // query head of the group this lane's logits belong to
+    const int hi = r16 >> 3, hh = r16 & 7;
     const int Hq = a.Hq, nc_max = a.nc_max;
     const int G = Hq / NW;
-    const int g = w;                  // KV head of this wave
-
-    Partials part(a.ws, a.hdr_bytes, a.L, nc_max, Hq);
-    // Work order: a single sequence's full chunks of every layer come first
-    // and the layers' short remainder chunks last, so the partial last round
-    // of workgroups is the cheap one.  A ragged call goes layer by layer.
-    const int item = blockIdx.x;
+    // item = (chunk item, KV head), KV head fastest; chunk items are ordered
+    // as in the attend kernel (a single sequence's full chunks of every layer
+    // first, its short remainders last)
+    const int g = static_cast<int>(blockIdx.x) % NW;
+    const int ci = static_cast<int>(blockIdx.x) / NW;
     int l, f;
     if constexpr (RAG) {
-        l = item / nc_max;
-        f = item - l * nc_max;
+        l = ci / nc_max;
+        f = ci - l * nc_max;
     } else {
         const int n_full = (a.len + 1) / CHUNK;
-        if (item < a.L * n_full) {
-            l = item / n_full;
-            f = item - l * n_full;
+        if (ci < a.L * n_full) {
+            l = ci / n_full;
+            f = ci - l * n_full;
         } else {
-            l = item - a.L * n_full;
+            l = ci - a.L * n_full;
             f = n_full;
         }
     }
     SeqItem it;
     int c;
     if (!resolve_chunk<RAG>(a, f, it, c)) return;
-    const int len = it.len;
-    const int T = len + 1;
+    const int len = it.len, T = len + 1;
     const int k_begin = chunk_begin(c);
     const int nk = chunk_keys(c, T);
+    const int kw0 = k_begin + VT * w;  // the wave's first key
+    const int rows = min(VT, max(nk - VT * w, 0));
     const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base) * D;
     uint16_t* Kh = a.k_cache + head_base;
     uint16_t* Vh = a.v_cache + head_base;
-    const size_t row_sl = static_cast<size_t>(it.s) * a.L + l;  // (sequence, layer) row of q, out, k_new, v_new
+    const size_t row_sl = static_cast<size_t>(it.s) * a.L + l;
 
-    // Eq. (1) first: the chunk holding slot len writes the new row into the
-    // cache (the wave of each KV head its own row, complete before its loads),
-    // so every key is read from the cache the same way.
-    if (len >= k_begin && len < k_begin + nk) {
+    // Eq. (1) first: the wave whose keys hold slot len writes the new row of
+    // its KV head before its loads (and KV head 0 the position).
+    if (len >= kw0 && len < kw0 + VT) {
         const uint16_t* kn = a.k_new + (row_sl * NW + g) * D;
         const uint16_t* vn = a.v_new + (row_sl * NW + g) * D;
         if (lane < 16)
@@ -179,51 +210,31 @@ __global__ __launch_bounds__(64 * NW, DEPTH == 1 ? ATTEND_WG_PER_CU : 1) void de
         else if (lane < 32)
             *reinterpret_cast<uint4*>(Vh + len * D + 8 * (lane - 16)) =
                 *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
-        if (tid == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
+        if (g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
         __threadfence_block();
     }
 
-    // Staging: the chunk's K rows and then its V rows stream through the
-    // registers as one sequence of 8 tiles of 32 rows.  Instruction m of a
-    // tile reads rows 4m..4m+3 whole (lane = row 4m + q4, 16-byte column r16)
-    // with buffer loads from a descriptor based at the tile's first row and
-    // bounded to the chunk's rows, so rows past the chunk end read as zero and
-    // cost no memory traffic (their logits are masked, their probabilities
-    // are zero).  The descriptor is scalar; every load shares the lane offset.
-    const uint16_t* const kc = Kh + static_cast<size_t>(k_begin) * D;
-    const uint16_t* const vc = Vh + static_cast<size_t>(k_begin) * D;
+    // both tiles requested at once; rows past the chunk read as zero without
+    // touching memory (bounded scalar descriptors)
     const int lane_off = q4 * (D * 2) + 16 * r16;
-    // tile tt: K tiles 0 .. PAIRS - 1, then V tiles; held in slot tt % DEPTH
-    uint4 stg[DEPTH][8];
-    auto load_tile = [&](int tt) {
-        const uint16_t* base = tt < PAIRS ? kc : vc;
-        const int u = tt % PAIRS;
-        const int rows = nk - VT * u > 0 ? nk - VT * u : 0;
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base) + VT * u * D, 0, rows * D * 2, kBufferDword3);
+    uint4 kt[8], vt[8];
+    {
+        const __amdgpu_buffer_rsrc_t rk =
+            __builtin_amdgcn_make_buffer_rsrc(Kh + static_cast<size_t>(kw0) * D, 0, rows * D * 2, kBufferDword3);
+        const __amdgpu_buffer_rsrc_t rv =
+            __builtin_amdgcn_make_buffer_rsrc(Vh + static_cast<size_t>(kw0) * D, 0, rows * D * 2, kBufferDword3);
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
-            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lane_off + 4 * m * (D * 2), 0, 0);
-            __builtin_memcpy(&stg[tt % DEPTH][m], &v, 16);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off + 4 * m * (D * 2), 0, 0);
+            __builtin_memcpy(&kt[m], &v, 16);
         }
-    };
 #pragma unroll
-    for (int tt = 0; tt < DEPTH; ++tt) load_tile(tt);
-
-    // Per-lane LDS bases.  Stores: lane (q4, r16) writes 16-byte column r16 of
-    // row 4m + q4 in instruction m.  K reads (A operand of S^T = K Q^T): row
-    // r16 (+16 for the odd tile), columns 4s + q4.  V reads (transposed B
-    // operand of P V): in each 16-lane group, row 4 q4 + r16 / 4 (+16 for
-    // keys 16..31 of the tile), 8 bytes at column 32 n + 16 ((r16 & 3) / 2) +
-    // 8 (r16 & 1).
-    uint8_t* const buf = s_tile[w];
-    uint8_t* const kw = buf + q4 * KSTRIDE + 16 * r16;
-    uint8_t* const vw = buf + q4 * VSTRIDE + 16 * r16;
-    const uint8_t* const kr = buf + r16 * KSTRIDE + 16 * q4;
-    const uint8_t* const vr = buf + (4 * q4 + (r16 >> 2)) * VSTRIDE + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
-
-    // ---------------- pass 1: logits S^T = K Q^T ----------------
-    uint4 qv[KSTEPS];  // B operand: Q^T, column r16 = query head (zero past G)
+        for (int m = 0; m < 8; ++m) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, lane_off + 4 * m * (D * 2), 0, 0);
+            __builtin_memcpy(&vt[m], &v, 16);
+        }
+    }
+    uint4 qv[KSTEPS];
     {
         const int hq = r16 < G ? r16 : 0;
         const uint16_t* qrow = a.q + (row_sl * Hq + g * G + hq) * D + 8 * q4;
@@ -233,136 +244,122 @@ __global__ __launch_bounds__(64 * NW, DEPTH == 1 ? ATTEND_WG_PER_CU : 1) void de
             qv[s] = (r16 < G) ? v : make_uint4(0, 0, 0, 0);
         }
     }
-    // sp[u][i]: lanes with hi = 0 hold key 32u + 4 q4 + i, head hh; lanes with
-    // hi = 1 hold key 32u + 16 + 4 q4 + i, head hh.
-    float sp[PAIRS][4];
+    uint8_t* const buf = s_tile[w];
+    uint8_t* const kwp = buf + q4 * KSTRIDE + 16 * r16;
+    uint8_t* const vwp = buf + q4 * VSTRIDE + 16 * r16;
+    const uint8_t* const kr = buf + r16 * KSTRIDE + 16 * q4;
+    const uint8_t* const vr = buf + (4 * q4 + (r16 >> 2)) * VSTRIDE + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
+
+    // ---- logits of the wave's 32 keys: S^T = K Q^T ----
 #pragma unroll
-    for (int u = 0; u < PAIRS; ++u) {
+    for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(kwp + 4 * KSTRIDE * m) = kt[m];
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
+    f32x4 acc[2];
 #pragma unroll
-        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(kw + 4 * KSTRIDE * m) = stg[u % DEPTH][m];
-        if (u + DEPTH < 2 * PAIRS) load_tile(u + DEPTH);  // the V tiles follow the K tiles
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
-        f32x4 acc[2];
+    for (int ti = 0; ti < 2; ++ti) {
+        acc[ti] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ti = 0; ti < 2; ++ti) {
-            acc[ti] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < KSTEPS; ++s) {
-                const uint4 a = *reinterpret_cast<const uint4*>(kr + 16 * KSTRIDE * ti + 64 * s);
-                acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qv[s]), acc[ti], 0, 0, 0);
-            }
+        for (int s = 0; s < KSTEPS; ++s) {
+            const uint4 av = *reinterpret_cast<const uint4*>(kr + 16 * KSTRIDE * ti + 64 * s);
+            acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(qv[s]), acc[ti], 0, 0, 0);
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float odd = ror8(acc[1][i]);  // lane hi=1 receives the odd tile of head hh
-            const float v = hi ? odd : acc[0][i];
-            const int key = VT * u + 16 * hi + 4 * q4 + i;
-            sp[u][i] = (key < nk) ? v * a.scale_log2 : -INFINITY;
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
     }
+    float sp[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float odd = ror8(acc[1][i]);
+        const float v = hi ? odd : acc[0][i];
+        const int key = VT * w + 16 * hi + 4 * q4 + i;  // within the chunk
+        sp[i] = (key < nk) ? v * a.scale_log2 : -INFINITY;
+    }
+    float m_w = fmaxf(fmaxf(sp[0], sp[1]), fmaxf(sp[2], sp[3]));
+    m_w = fmaxf(m_w, __shfl_xor(m_w, 16, 64));
+    m_w = fmaxf(m_w, __shfl_xor(m_w, 32, 64));
+    m_w = fmaxf(m_w, ror8(m_w));
+    if (q4 == 0 && hi == 0) s_m[w][hh] = m_w;
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // the K tile's reads are done: the V tile takes the buffer
+#pragma unroll
+    for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vwp + 4 * VSTRIDE * m) = vt[m];
+    __syncthreads();
 
-    // ---------------- chunk statistics ----------------
-    // per head hh (8 lanes share it: q4 x hi); afterwards sp holds p~ = exp2(s - m_c)
-    float m_c = -INFINITY;
+    // ---- the chunk's max per head, p~ against it ----
+    float m_c = s_m[0][hh];
 #pragma unroll
-    for (int u = 0; u < PAIRS; ++u)
+    for (int v = 1; v < SPLIT_W; ++v) m_c = fmaxf(m_c, s_m[v][hh]);
+    float l_w = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) m_c = fmaxf(m_c, sp[u][i]);
-    m_c = fmaxf(m_c, __shfl_xor(m_c, 16, 64));
-    m_c = fmaxf(m_c, __shfl_xor(m_c, 32, 64));
-    m_c = fmaxf(m_c, ror8(m_c));
-    float l_c = 0.f;
-#pragma unroll
-    for (int u = 0; u < PAIRS; ++u)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            sp[u][i] = exp2f(sp[u][i] - m_c);
-            l_c += sp[u][i];
-        }
-    l_c += __shfl_xor(l_c, 16, 64);
-    l_c += __shfl_xor(l_c, 32, 64);
-    l_c += ror8(l_c);
-    const int pbase = (l * nc_max + it.first + c) * Hq + g * G;  // < 2^31 (checked on the host)
-    if (q4 == 0 && r16 < G) part.ml[pbase + r16] = make_float2(m_c, l_c);
+    for (int i = 0; i < 4; ++i) {
+        sp[i] = exp2f(sp[i] - m_c);
+        l_w += sp[i];
+    }
+    l_w += __shfl_xor(l_w, 16, 64);
+    l_w += __shfl_xor(l_w, 32, 64);
+    l_w += ror8(l_w);
+    if (q4 == 0 && hi == 0) s_l[w][hh] = l_w;
+    const uint32_t p01 = pack_bf16x2(sp[0], sp[1]), p23 = pack_bf16x2(sp[2], sp[3]);
+    if (hh < G) *reinterpret_cast<uint2*>(&s_p[hh][VT * w + 16 * hi + 4 * q4]) = make_uint2(p01, p23);
 
-    // ---------------- pass 2: O^T = V^T P^T on the matrix cores ----------------
-    // (D tile n: column = head r16, rows = channels 16 n + 4 q4 + 0..3, so each
-    // lane ends with runs of 4 channels of one head)
+    // ---- O^T = V^T P^T over the wave's keys ----
+    float ev[4], od[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float x = sp[i];
+        const float y = ror8(x);
+        ev[i] = hi ? y : x;
+        od[i] = hi ? x : y;
+    }
+    const uint4 pw = make_uint4(pack_bf16x2(ev[0], ev[1]), pack_bf16x2(ev[2], ev[3]), pack_bf16x2(od[0], od[1]),
+                                pack_bf16x2(od[2], od[3]));
+    const bf16x8_t pa = as_bf16x8(pw);
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     f32x4 oacc[DTILES];
 #pragma unroll
-    for (int n = 0; n < DTILES; ++n) oacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int u = 0; u < PAIRS; ++u) {
-#pragma unroll
-        for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vw + 4 * VSTRIDE * m) = stg[(PAIRS + u) % DEPTH][m];
-        if (PAIRS + u + DEPTH < 2 * PAIRS) load_tile(PAIRS + u + DEPTH);
-        // B operand P^T: column = head r16 (columns >= G feed output columns
-        // that are never stored), k-slots 8 q4 + i -> keys 32u + 4 q4 + i (i < 4)
-        // and 32u + 16 + 4 q4 + i - 4 (i >= 4): the even tile is in place, the
-        // odd tile comes back from the upper half of the row.
-        float ev[4], od[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float x = sp[u][i];
-            const float y = ror8(x);
-            ev[i] = hi ? y : x;
-            od[i] = hi ? x : y;
-        }
-        const uint4 pw = make_uint4(pack_bf16x2(ev[0], ev[1]), pack_bf16x2(ev[2], ev[3]), pack_bf16x2(od[0], od[1]),
-                                    pack_bf16x2(od[2], od[3]));
-        const bf16x8_t pa = as_bf16x8(pw);
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
-#pragma unroll
-        for (int n = 0; n < DTILES; ++n) {
-            s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vr + 32 * n));
-            s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) s16x4*)(vr + 16 * VSTRIDE + 32 * n));
-            uint4 bw;
-            __builtin_memcpy(&bw.x, &b0, 8);
-            __builtin_memcpy(&bw.z, &b1, 8);
-            oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(bw), pa, oacc[n], 0, 0, 0);
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the next tile is stored
+    for (int n = 0; n < DTILES; ++n) {
+        s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(vr + 32 * n));
+        s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(vr + 16 * VSTRIDE + 32 * n));
+        uint4 bw;
+        __builtin_memcpy(&bw.x, &b0, 8);
+        __builtin_memcpy(&bw.z, &b1, 8);
+        oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(bw), pa, zero, 0, 0, 0);
     }
-    // ---------------- partial results: whole rows through LDS ----------------
-    // p~ (bfloat16, CHUNK entries per head) and O (bfloat16 relative to the chunk
-    // max, 256 bytes per head) of the wave's G heads are staged in its free
-    // tile buffer at padded per-head strides, then written as 1 KB fully
-    // coalesced stores: the workspace holds both as rows, heads of the wave
-    // adjacent.
+    __syncthreads();  // every wave's V reads are done: the tiles take the partial outputs
+    float* const s_o = reinterpret_cast<float*>(&s_tile[0][0]);  // [SPLIT_W][GMAX][OS]
+    if (r16 < G) {
+#pragma unroll
+        for (int n = 0; n < DTILES; ++n)
+            *reinterpret_cast<f32x4*>(s_o + (w * GMAX + r16) * OS + 16 * n + 4 * q4) = oacc[n];
+    }
+    __syncthreads();
+
+    // ---- partial results of (chunk, head): (m_c, l_c), O_c and p~ ----
+    Partials part(a.ws, a.hdr_bytes, a.L, nc_max, Hq);
+    const int pbase = (l * nc_max + it.first + c) * Hq + g * G;  // < 2^31 (checked on the host)
+    if (tid < G) {
+        float lc = 0.f;
+#pragma unroll
+        for (int v = 0; v < SPLIT_W; ++v) lc += s_l[v][tid];
+        float mc = s_m[0][tid];
+#pragma unroll
+        for (int v = 1; v < SPLIT_W; ++v) mc = fmaxf(mc, s_m[v][tid]);
+        part.ml[pbase + tid] = make_float2(mc, lc);
+    }
     {
-        constexpr int PR = CHUNK * 2, HSP = PR + 64, HS = 256 + 64;
-        static_assert(GMAX * (HSP + HS) <= TILE_BYTES, "the staged partials fit in the tile buffer");
-        uint8_t* const lp = buf;
-        uint8_t* const lo = buf + GMAX * HSP;
-        if (hh < G) {
+        // 4 channels (outputs) or 4 keys (p~) per thread, whole rows per head
+        const int h = tid >> 5, c4 = 4 * (tid & 31);
+        if (h < G) {
+            float o[4];
 #pragma unroll
-            for (int u = 0; u < PAIRS; ++u)
-                *reinterpret_cast<uint2*>(lp + hh * HSP + 2 * (VT * u + 16 * hi + 4 * q4)) =
-                    make_uint2(pack_bf16x2(sp[u][0], sp[u][1]), pack_bf16x2(sp[u][2], sp[u][3]));
-        }
-        if (r16 < G) {
+            for (int e = 0; e < 4; ++e) {
+                float x = 0.f;
 #pragma unroll
-            for (int n = 0; n < DTILES; ++n)
-                *reinterpret_cast<uint2*>(lo + r16 * HS + 2 * (16 * n + 4 * q4)) =
-                    make_uint2(pack_bf16x2(oacc[n][0], oacc[n][1]), pack_bf16x2(oacc[n][2], oacc[n][3]));
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): staged
-        uint8_t* const gp = reinterpret_cast<uint8_t*>(part.p) + static_cast<size_t>(pbase) * PR;
-        uint8_t* const go = reinterpret_cast<uint8_t*>(part.o) + static_cast<size_t>(pbase) * (D * 2);
-#pragma unroll
-        for (int j = 0; j < GMAX * PR / 1024; ++j) {
-            const int off = 1024 * j + 16 * lane;
-            if (off < G * PR)
-                *reinterpret_cast<uint4*>(gp + off) =
-                    *reinterpret_cast<const uint4*>(lp + (off / PR) * HSP + off % PR);
-        }
-#pragma unroll
-        for (int j = 0; j < GMAX * 256 / 1024; ++j) {
-            const int off = 1024 * j + 16 * lane;
-            if (off < G * 256)
-                *reinterpret_cast<uint4*>(go + off) = *reinterpret_cast<const uint4*>(lo + (off >> 8) * HS + (off & 255));
+                for (int v = 0; v < SPLIT_W; ++v) x += s_o[(v * GMAX + h) * OS + c4 + e];
+                o[e] = x;
+            }
+            *reinterpret_cast<uint2*>(part.o + static_cast<size_t>(pbase + h) * D + c4) =
+                make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+            *reinterpret_cast<uint2*>(part.p + static_cast<size_t>(pbase + h) * CHUNK + c4) =
+                *reinterpret_cast<const uint2*>(&s_p[h][c4]);
         }
     }
 }
@@ -467,9 +464,12 @@ __device__ void output_block(const FusedArgs& a, int h, int l, int s_arg, bool s
     int s = 0, first = 0, n_chunks = a.n_chunks;
     if constexpr (RAG) {
         s = s_arg;
+        // the sequence's own values and the earlier sequences' chunk counts
+        // are loaded side by side (one round of loads)
         const int st = vz::ragged_decode_status(a.rag, s);
-        first = st == VZ_OK ? vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); }) : -1;
-        n_chunks = st == VZ_OK ? ragged_chunks(a.rag, s) : 0;
+        const int fst = vz::ragged_first(s, a.nc_max, [&](int u) { return ragged_chunks(a.rag, u); });
+        first = st == VZ_OK ? fst : -1;
+        n_chunks = st == VZ_OK ? (a.rag.len[s] + CHUNK) / CHUNK : 0;
         const bool ok = st == VZ_OK && first >= 0 && first + n_chunks <= a.nc_max;
         if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[s] = ok ? VZ_OK : (st != VZ_OK ? st : VZ_ERR_CAPACITY);
         if (!ok) return;
@@ -685,12 +685,7 @@ hipError_t launch_decode_fused(const VzDecodeArgs& v, hipStream_t stream) {
         }
         return vz_launch_decode_range(a, NW, stream);
     }
-    // grids of at most two workgroups per CU: four tiles in flight per wave
-    // (all eight measured slower: their registers spill into the AGPRs)
-    if (static_cast<int64_t>(a.L) * a.n_chunks <= ATTEND_DEEP_MAX_ITEMS)
-        hipLaunchKernelGGL((decode_attend_kernel<NW, RAG, PAIRS>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
-    else
-        hipLaunchKernelGGL((decode_attend_kernel<NW, RAG, 1>), dim3(a.L * a.n_chunks), dim3(64 * NW), 0, stream, a);
+    hipLaunchKernelGGL((decode_attend_kernel<NW, RAG>), dim3(a.L * a.n_chunks * NW), dim3(64 * SPLIT_W), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((a.plane + CHUNK - 1) / CHUNK <= FINISH_MAX_CHUNKS) {

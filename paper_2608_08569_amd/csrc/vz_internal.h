@@ -138,15 +138,17 @@ constexpr int32_t kRaggedMaxSeqs = 1 << 15;  // also a grid dimension
 
 namespace vz {
 
-// Status of sequence s for a decode step: VZ_OK when slot len[s] exists and
-// the sequence lies inside the planes, VZ_IDLE for an idle slot (cap 0).
-__device__ __forceinline__ int ragged_decode_status(const VzRagged& r, int s) {
-    const int64_t b = r.base[s];
-    const int c = r.cap[s], n = r.len[s], p = r.next_pos[s];
+// Status of a sequence for a decode step from its values (base, cap, len,
+// next_pos): VZ_OK when slot len exists and the sequence lies inside the
+// planes of `total` slots, VZ_IDLE for an idle slot (cap 0).
+__device__ __forceinline__ int decode_status_of(int64_t b, int c, int n, int p, int64_t total) {
     if (c == 0) return VZ_IDLE;
-    if (n < 0 || p < 0 || c < 1 || b < 0 || b > r.total - c) return VZ_ERR_INVALID;
+    if (n < 0 || p < 0 || c < 1 || b < 0 || b > total - c) return VZ_ERR_INVALID;
     if (n >= c) return VZ_ERR_CAPACITY;  // no free slot (len + 1 > cap, without overflow)
     return VZ_OK;
+}
+__device__ __forceinline__ int ragged_decode_status(const VzRagged& r, int s) {
+    return decode_status_of(r.base[s], r.cap[s], r.len[s], r.next_pos[s], r.total);
 }
 
 // Flat work items of a ragged batch: sequence s contributes count(s) >= 0

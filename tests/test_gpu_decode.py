@@ -185,10 +185,9 @@ def test_many_chunks_per_layer():
 
 
 def test_small_and_large_chunked_grids_agree():
-    """A chunked call over 20 layers (32 chunks each: 640 workgroups, one tile
-    in flight per wave) and one-layer calls of the same data (32 workgroups,
-    four tiles in flight) give the same bits; the first layer also against
-    the oracle."""
+    """A chunked call over 20 layers (32 chunks each: 2560 workgroups) and
+    one-layer calls of the same data (128 workgroups) give the same bits; the
+    first layer also against the oracle."""
     dtype, L, Hq, Hkv, d, length = synth.DT_BF16, 20, 32, 4, 128, 4000
     k, v, s, p = synth.random_state(14, L, Hkv, d, length + 2, length, dtype, next_pos=length + 9)
     key = synth.stream_key(14, "grids")
