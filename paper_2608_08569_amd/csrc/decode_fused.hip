@@ -386,53 +386,36 @@ __device__ __forceinline__ float2 combine_rows(const float* sm, const float* sl,
     return make_float2(Mg, 1.0f / sum);
 }
 
-// Output row of head h of (layer l, sequence s) from the sequence's n_chunks
-// partials starting at chunk row `first`, by a whole block of OUT_THREADS
-// threads.  Thread t owns channels 8 (t % 16) .. +7 of the rows of chunks
-// t / 16, t / 16 + 16, ...: a running max, o = sum_c O_c exp2(m_c - M) /
-// sum_c l_c exp2(m_c - M); the 16 row groups then merge in LDS.  All loads of
-// a round (16-byte row pieces and the chunk pairs) are issued before any use:
-// indexes past the end are clamped and the values masked afterwards.
-// Returns the layer's (max, 1 / sum) of head h in thread 0.
-__device__ float2 merge_output_row(const FusedArgs& a, const Partials& part, int h, int l, int s, int first,
-                                   int n_chunks) {
+// One round of a row group's chunks: chunk c0 + OUT_ROWS k of pair st[k] and
+// row piece xr[k], while it is below n_chunks, into the running (M, S, acc).
+__device__ __forceinline__ void merge_batch(const float2 (&st)[OUT_BATCH], const uint4 (&xr)[OUT_BATCH], int c0,
+                                            int n_chunks, float& M, float& S, float (&acc)[8]) {
+#pragma unroll
+    for (int k = 0; k < OUT_BATCH; ++k) {
+        if (c0 + OUT_ROWS * k >= n_chunks) break;
+        if (st[k].x > M) {
+            const float r = exp2f(M - st[k].x);  // 0 while M is -inf
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] *= r;
+            S *= r;
+            M = st[k].x;
+        }
+        const float wgt = exp2f(st[k].x - M);
+        float x[8];
+        vz::unpack16<VZ_BF16>(xr[k], x);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(wgt, x[i], acc[i]);
+        S = fmaf(wgt, st[k].y, S);
+    }
+}
+
+// The 16 row groups' (M, S, acc) merged in LDS, the output row stored;
+// returns the layer's (max, 1 / sum) of head h in thread 0.
+__device__ float2 merge_rows_store(const FusedArgs& a, int h, int l, int s, float M, float S, const float (&acc)[8]) {
     __shared__ float s_acc[OUT_ROWS][D + 4];
     __shared__ float s_m[OUT_ROWS], s_l[OUT_ROWS];
     const int t = threadIdx.x, Hq = a.Hq;
     const int rg = t / 16, c8 = 8 * (t % 16);
-    const size_t row0 = static_cast<size_t>(l) * a.nc_max + first;  // first chunk row of (layer, sequence)
-    const float2* ml = part.ml + row0 * Hq + h;
-    const uint16_t* po = part.o + (row0 * Hq + h) * D + c8;
-    float M = -INFINITY, S = 0.f, acc[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-    for (int c0 = rg; c0 < n_chunks; c0 += OUT_ROWS * OUT_BATCH) {
-        float2 st[OUT_BATCH];
-        uint4 xr[OUT_BATCH];
-#pragma unroll
-        for (int k = 0; k < OUT_BATCH; ++k) {
-            const int cc = min(c0 + OUT_ROWS * k, n_chunks - 1);
-            st[k] = ml[static_cast<size_t>(cc) * Hq];
-            xr[k] = *reinterpret_cast<const uint4*>(po + static_cast<size_t>(cc) * Hq * D);
-        }
-#pragma unroll
-        for (int k = 0; k < OUT_BATCH; ++k) {
-            if (c0 + OUT_ROWS * k >= n_chunks) break;
-            if (st[k].x > M) {
-                const float r = exp2f(M - st[k].x);  // 0 while M is -inf
-#pragma unroll
-                for (int i = 0; i < 8; ++i) acc[i] *= r;
-                S *= r;
-                M = st[k].x;
-            }
-            const float wgt = exp2f(st[k].x - M);
-            float x[8];
-            vz::unpack16<VZ_BF16>(xr[k], x);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) acc[i] = fmaf(wgt, x[i], acc[i]);
-            S = fmaf(wgt, st[k].y, S);
-        }
-    }
 #pragma unroll
     for (int i = 0; i < 8; ++i) s_acc[rg][c8 + i] = acc[i];
     if (t % 16 == 0) {
@@ -453,6 +436,76 @@ __device__ float2 merge_output_row(const FusedArgs& a, const Partials& part, int
         a.out[(row_sl * Hq + h) * D + t] = vz::f32_to_bf16(o * stats.y);
     }
     return stats;
+}
+
+// Loads of one round: the pairs and row pieces of chunks c0 + OUT_ROWS k,
+// rows clamped to n_load - 1 (every load in bounds, the values masked later).
+__device__ __forceinline__ void merge_load(const float2* ml, const uint16_t* po, int Hq, int c0, int n_load,
+                                           float2 (&st)[OUT_BATCH], uint4 (&xr)[OUT_BATCH]) {
+#pragma unroll
+    for (int k = 0; k < OUT_BATCH; ++k) {
+        const int cc = min(c0 + OUT_ROWS * k, n_load - 1);
+        st[k] = ml[static_cast<size_t>(cc) * Hq];
+        xr[k] = *reinterpret_cast<const uint4*>(po + static_cast<size_t>(cc) * Hq * D);
+    }
+}
+
+// Output row of head h of (layer l, sequence s) from the sequence's n_chunks
+// partials starting at chunk row `first`, by a whole block of OUT_THREADS
+// threads.  Thread t owns channels 8 (t % 16) .. +7 of the rows of chunks
+// t / 16, t / 16 + 16, ...: a running max, o = sum_c O_c exp2(m_c - M) /
+// sum_c l_c exp2(m_c - M); the 16 row groups then merge in LDS.  All loads of
+// a round (16-byte row pieces and the chunk pairs) are issued before any use:
+// indexes past the end are clamped and the values masked afterwards.
+// Returns the layer's (max, 1 / sum) of head h in thread 0.
+__device__ float2 merge_output_row(const FusedArgs& a, const Partials& part, int h, int l, int s, int first,
+                                   int n_chunks) {
+    const int t = threadIdx.x, Hq = a.Hq;
+    const int rg = t / 16, c8 = 8 * (t % 16);
+    const size_t row0 = static_cast<size_t>(l) * a.nc_max + first;  // first chunk row of (layer, sequence)
+    const float2* ml = part.ml + row0 * Hq + h;
+    const uint16_t* po = part.o + (row0 * Hq + h) * D + c8;
+    float M = -INFINITY, S = 0.f, acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+    for (int c0 = rg; c0 < n_chunks; c0 += OUT_ROWS * OUT_BATCH) {
+        float2 st[OUT_BATCH];
+        uint4 xr[OUT_BATCH];
+        merge_load(ml, po, Hq, c0, n_chunks, st, xr);
+        merge_batch(st, xr, c0, n_chunks, M, S, acc);
+    }
+    return merge_rows_store(a, h, l, s, M, S, acc);
+}
+
+// Output block of a call of one sequence whose planes hold at most
+// OUT_ROWS * OUT_BATCH chunks (one round): its chunk rows start at row 0, so
+// the round's loads (rows clamped to the layer's n_load rows) go out before
+// the sequence's values arrive, and the same arithmetic as merge_output_row
+// follows.  A ragged call of one sequence reports its status here (head 0 of
+// layer 0).
+template <bool RAG>
+__device__ void output_block_one(const FusedArgs& a, int h, int l) {
+    const int t = threadIdx.x, Hq = a.Hq;
+    const int rg = t / 16, c8 = 8 * (t % 16);
+    Partials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
+    const size_t row0 = static_cast<size_t>(l) * a.nc_max;
+    float2 st[OUT_BATCH];
+    uint4 xr[OUT_BATCH];
+    merge_load(part.ml + row0 * Hq + h, part.o + (row0 * Hq + h) * D + c8, Hq, rg, RAG ? a.nc_max : a.n_chunks, st,
+               xr);
+    int n_chunks = a.n_chunks;
+    if constexpr (RAG) {
+        const int st0 = vz::ragged_decode_status(a.rag, 0);
+        n_chunks = st0 == VZ_OK ? (a.rag.len[0] + CHUNK) / CHUNK : 0;
+        const bool ok = st0 == VZ_OK && n_chunks <= a.nc_max;
+        if (a.rag.status && h == 0 && l == 0 && t == 0) a.rag.status[0] = ok ? VZ_OK : (st0 != VZ_OK ? st0 : VZ_ERR_CAPACITY);
+        if (!ok) return;
+    }
+    float M = -INFINITY, S = 0.f, acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+    merge_batch(st, xr, rg, n_chunks, M, S, acc);
+    merge_rows_store(a, h, l, 0, M, S, acc);
 }
 
 // Output kernel, one block per (head, layer, sequence):
@@ -546,17 +599,21 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
     __shared__ float2 s_stat[FINISH_MAX_HEADS];
     __shared__ float s_f[FOLD_HEADS];
     const int t = threadIdx.x, l = blockIdx.y, Hq = a.Hq;
+    // One sequence (a single-sequence call, or a ragged call of one): its
+    // chunk rows start at row 0 of the layer and a fold block's chunk is row
+    // blockIdx.x, so every partial-result load is issued before the
+    // sequence's values are known (rows clamped to the layer's rows, values
+    // masked once they are): one round of loads instead of two.
+    const bool one = !RAG || a.rag.n == 1;
     if (static_cast<int>(blockIdx.x) >= a.n_chunks) {
         const int ob = static_cast<int>(blockIdx.x) - a.n_chunks;
-        output_block<RAG>(a, ob % Hq, l, ob / Hq, false);
+        if (one)
+            output_block_one<RAG>(a, ob % Hq, l);
+        else
+            output_block<RAG>(a, ob % Hq, l, ob / Hq, false);
         return;
     }
-    SeqItem it;
-    int c;
-    if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) return;
     const ConstPartials part(a.ws, a.hdr_bytes, a.L, a.nc_max, Hq);
-    const size_t row0 = static_cast<size_t>(l) * a.nc_max + it.first;
-    const int nch = it.n_chunks;
     // Loads first, all independent of one another: the chunk pairs of the
     // statistics (thread t: (head, row group) pairs t, t + OUT_THREADS, ...,
     // up to FINISH_GROUP_CHUNKS chunks each, indexes clamped), the fold's p~
@@ -564,26 +621,75 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
     constexpr int FINISH_GROUP_CHUNKS = FINISH_MAX_CHUNKS / OUT_ROWS;
     constexpr int FINISH_PAIRS = FINISH_MAX_HEADS * OUT_ROWS / OUT_THREADS;
     float2 stv[FINISH_PAIRS][FINISH_GROUP_CHUNKS];
+    uint16_t pr[FOLD_HEADS];
+    float m_own;
+    const int tk = t < CHUNK ? t : 0;
+    // (head, row group) pair pi = rg * Hq + h: the 64 lanes of a load
+    // instruction read whole rows of heads (two rows of 32 heads, four cache
+    // lines); rounds past the Hq * OUT_ROWS pairs are skipped (uniform)
+    auto load_pairs = [&](size_t row0, int n_load) {
 #pragma unroll
-    for (int u = 0; u < FINISH_PAIRS; ++u) {
-        const int pi = min(t + u * OUT_THREADS, Hq * OUT_ROWS - 1);
-        const int h = pi / OUT_ROWS, rg = pi - h * OUT_ROWS;
+        for (int u = 0; u < FINISH_PAIRS; ++u) {
+            if (u * OUT_THREADS >= Hq * OUT_ROWS) break;
+            const int pi = min(t + u * OUT_THREADS, Hq * OUT_ROWS - 1);
+            const int rg = pi / Hq, h = pi - rg * Hq;
 #pragma unroll
-        for (int k = 0; k < FINISH_GROUP_CHUNKS; ++k)
-            stv[u][k] = part.ml[(row0 + min(rg + k * OUT_ROWS, nch - 1)) * Hq + h];
+            for (int k = 0; k < FINISH_GROUP_CHUNKS; ++k)
+                stv[u][k] = part.ml[(row0 + min(rg + k * OUT_ROWS, n_load - 1)) * Hq + h];
+        }
+    };
+    auto load_own = [&](size_t cbase) {
+        const uint16_t* pp = part.p + cbase * CHUNK + tk;
+#pragma unroll
+        for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(q, Hq - 1) * CHUNK];
+        m_own = part.ml[cbase + min(t % FOLD_HEADS, Hq - 1)].x;
+    };
+    SeqItem it;
+    int c;
+    if (one) {
+        // the sequence's values first (a ragged call of one: sequence 0 owns
+        // chunk rows [0, its chunks)), then the partial results, then the
+        // checks: the score load below waits only for the values
+        int64_t b = 0;
+        int cp = a.plane, ln = a.len, np = a.next_pos;
+        if constexpr (RAG) {
+            b = a.rag.base[0];
+            cp = a.rag.cap[0];
+            ln = a.rag.len[0];
+            np = a.rag.next_pos[0];
+        }
+        load_pairs(static_cast<size_t>(l) * a.nc_max, RAG ? a.nc_max : a.n_chunks);
+        load_own((static_cast<size_t>(l) * a.nc_max + blockIdx.x) * Hq);
+        int nc = a.n_chunks;
+        if constexpr (RAG) {
+            const bool ok = vz::decode_status_of(b, cp, ln, np, a.rag.total) == VZ_OK;
+            nc = ok ? (ln + CHUNK) / CHUNK : 0;
+            if (nc > a.nc_max) nc = 0;
+        }
+        if (static_cast<int>(blockIdx.x) >= nc) return;
+        it.s = 0;
+        it.len = ln;
+        it.next_pos = np;
+        it.n_chunks = nc;
+        it.first = 0;
+        it.base = b;
+        c = blockIdx.x;
+    } else if (!resolve_chunk<RAG>(a, blockIdx.x, it, c)) {
+        return;
+    }
+    const size_t row0 = static_cast<size_t>(l) * a.nc_max + it.first;
+    const int nch = it.n_chunks;
+    const size_t cbase = (row0 + c) * Hq;  // = (layer row + blockIdx.x) * Hq
+    if (!one) {
+        load_pairs(row0, nch);
+        load_own(cbase);
     }
     const int len = it.len, T = len + 1;
     const int nk = chunk_keys(c, T);
-    const int tk = t < CHUNK ? t : 0;
     const int j = chunk_begin(c) + (tk < nk ? tk : 0);
     float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
     const float a_ld = *sc;
-    const size_t cbase = (row0 + c) * Hq;
     const uint16_t* pp = part.p + cbase * CHUNK + tk;
-    uint16_t pr[FOLD_HEADS];
-#pragma unroll
-    for (int q = 0; q < FOLD_HEADS; ++q) pr[q] = pp[min(q, Hq - 1) * CHUNK];
-    const float m_own = part.ml[cbase + min(t % FOLD_HEADS, Hq - 1)].x;
 
     // the layer statistics of every head: row group rg of head h takes
     // chunks rg, rg + OUT_ROWS, ... with a running max, then the groups merge
@@ -591,7 +697,7 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
     for (int u = 0; u < FINISH_PAIRS; ++u) {
         const int pi = t + u * OUT_THREADS;
         if (pi < Hq * OUT_ROWS) {
-            const int rg = pi % OUT_ROWS;
+            const int rg = pi / Hq, h = pi - rg * Hq;
             float M = -INFINITY, S = 0.f;
 #pragma unroll
             for (int k = 0; k < FINISH_GROUP_CHUNKS; ++k) {
@@ -603,8 +709,8 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
                 }
                 S = fmaf(exp2f(st.x - M), st.y, S);
             }
-            s_gm[pi] = M;
-            s_gl[pi] = S;
+            s_gm[h * OUT_ROWS + rg] = M;
+            s_gl[h * OUT_ROWS + rg] = S;
         }
     }
     __syncthreads();
