@@ -507,6 +507,122 @@ def other_workload(args, torch, vz):
     }), flush=True)
 
 
+def serve_workload(args, torch, vz):
+    """Continuous batching (paper_2608_08569_amd.loop): a stream of requests
+    served through 16 batch slots of one packed cache.  Each request has the
+    batched workload's shape (48 layers, 32Q/4KV, d = 128, bf16, audio of
+    2k-32k tokens with spans of mean length 4, budget len / 4, eviction every
+    16 of its own steps) and generates 64-256 tokens; when it has generated
+    them it leaves, and the next waiting request is admitted into the freed
+    slot (its prefill fused there, Sec. 3.2.1).  Every step is one graph
+    replay (decode of all active slots + eviction when some slot is due).
+    All prefill caches and per-step inputs are drawn on the GPU and resident
+    before the timed region; the value is generated tokens per second over
+    the whole stream, admissions included."""
+    from paper_2608_08569_amd.loop import DecodeLoop
+    L, Hq, Hkv, d, interval, gamma = 48, 32, 4, 128, 16, 0.95
+    n_slots, n_req = 16, args.serve_requests
+    key = synth.stream_key(0, "serve16")
+    T_audio = synth.uniform_int(synth.stream_key(key, "lengths"), 0, n_req, 2048, 32768).astype(np.int64)
+    gen_len = synth.uniform_int(synth.stream_key(key, "generate"), 0, n_req, 64, 256).astype(np.int64)
+    offs = [synth.offsets_from_lengths(synth.spans_geometric(synth.stream_key(key, "spans", i), int(T), 0.25, 32))
+            for i, T in enumerate(T_audio)]
+    n_spans = np.array([len(o) - 1 for o in offs], dtype=np.int64)
+    budgets = T_audio // 4
+    cap = int(np.max(np.maximum(n_spans, budgets))) + interval + 1
+    t0 = time.time()
+    bf = torch.bfloat16
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(key & 0x7FFFFFFFFFFFFFFF)
+    rn = lambda *shape: torch.randn(*shape, generator=gen, device="cuda", dtype=torch.float32).to(bf)
+    pre = [(rn(L, Hkv, int(T), d), rn(L, Hkv, int(T), d)) for T in T_audio]
+    offs_d = [torch.from_numpy(o).cuda() for o in offs]
+    G = int(gen_len.max())
+    Q = rn(n_req * G, L, Hq, d)
+    KN = rn(n_req * G, L, Hkv, d)
+    VN = rn(n_req * G, L, Hkv, d)
+    lp = DecodeLoop(L, Hq, Hkv, d, [cap] * n_slots, [1] * n_slots, gamma, interval=interval)
+    qb = torch.zeros(n_slots, L, Hq, d, dtype=bf, device="cuda")
+    kb = torch.zeros(n_slots, L, Hkv, d, dtype=bf, device="cuda")
+    vb = torch.zeros_like(kb)
+    # input row of each slot's step: its request's first row plus the slot's
+    # device-side step count (no host-to-device copy per step)
+    idx = torch.zeros(n_slots, dtype=torch.int64, device="cuda")
+    slot_row0 = torch.zeros(n_slots, dtype=torch.int64, device="cuda")
+    for s in range(n_slots):
+        lp.retire(s)
+    lp.capture(qb, kb, vb)
+    torch.cuda.synchronize()
+    log(f"[gpu] serve16: {n_req} requests ({int(T_audio.sum())} audio tokens, {int(gen_len.sum())} to generate), "
+        f"slot capacity {cap}, inputs ready in {time.time() - t0:.1f}s")
+
+    def run():
+        """The whole stream; returns (generated tokens, algorithmic bytes, steps)."""
+        waiting = list(range(n_req))
+        holder = {}  # slot -> [request, tokens generated, resident length (host mirror)]
+        tokens = path_bytes = steps = 0
+        while waiting or holder:
+            for s in list(holder):
+                i, g, _ = holder[s]
+                if g == gen_len[i]:
+                    lp.retire(s)
+                    del holder[s]
+            for s in range(n_slots):
+                if s not in holder and waiting:
+                    i = waiting.pop(0)
+                    lp.admit(s, pre[i][0], pre[i][1], offs_d[i], budget=int(budgets[i]))
+                    slot_row0[s] = i * G
+                    holder[s] = [i, 0, int(n_spans[i])]
+            if not holder:
+                break
+            torch.add(slot_row0, lp.age, out=idx)
+            idx.clamp_(0, n_req * G - 1)  # idle slots count on; their rows are never used
+            torch.index_select(Q, 0, idx, out=qb)
+            torch.index_select(KN, 0, idx, out=kb)
+            torch.index_select(VN, 0, idx, out=vb)
+            lp.replay()
+            steps += 1
+            for s, h in holder.items():
+                i, g, ln = h
+                T = ln + 1
+                path_bytes += L * decode_bytes_per_layer(T, Hq, Hkv, d, 2)
+                if (g + 1) % interval == 0 and T > budgets[i]:
+                    path_bytes += L * evict_bytes_per_layer(T, T - int(budgets[i]), Hkv, d, 2)
+                    T = int(budgets[i])
+                h[1], h[2] = g + 1, T
+                tokens += 1
+        return tokens, path_bytes, steps
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    tokens = path_bytes = steps = 0
+    for _ in range(args.steps):
+        tk, b, st = run()
+        tokens += tk
+        path_bytes += b
+        steps += st
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    print(json.dumps({
+        "metric": "decode attend+score+evict tokens/s and HBM GB/s (% of peak)",
+        "value": tokens / elapsed, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "serve16",
+                   "description": (f"continuous batching: {n_req} requests of 2k-32k audio tokens (spans of mean "
+                                   f"length 4, budget len/4, eviction every 16 of their own steps) generating "
+                                   f"64-256 tokens each, through 16 batch slots of one packed cache; a request "
+                                   f"leaves when done and the next is admitted (prefill fused into the freed "
+                                   f"slot); one graph replay per step; one step = the whole stream"),
+                   "layers": L, "slots": n_slots, "requests": n_req, "generated_tokens": tokens // args.steps,
+                   "decode_steps": steps // args.steps},
+        "path_gbps": path_bytes / elapsed / 1e9,
+        "path_frac_of_hbm_peak": path_bytes / elapsed / 1e9 / HBM_PEAK_GBS,
+    }), flush=True)
+
+
 def loop_workload(args, torch, vz):
     """long32k through the decode loop (paper_2608_08569_amd.loop): one
     decode call per layer, layer l's query being its own input query plus
@@ -616,8 +732,9 @@ def main():
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--workload", default="long32k",
-                    choices=["long32k", "aggr64k", "batch16", "long32k-layers", "long32k-graph"],
+                    choices=["long32k", "aggr64k", "batch16", "long32k-layers", "long32k-graph", "serve16"],
                     help="long32k is the headline; the others are reported beside it")
+    ap.add_argument("--serve-requests", type=int, default=48, help="requests in the serve16 stream")
     ap.add_argument("--batch-streams", action="store_true",
                     help="batch16 with one stream and one call sequence per sequence instead of the ragged calls")
     args = ap.parse_args()
@@ -654,6 +771,9 @@ def main():
 
     if args.workload in ("long32k-layers", "long32k-graph"):
         loop_workload(args, torch, vz)
+        return
+    if args.workload == "serve16":
+        serve_workload(args, torch, vz)
         return
     if args.workload != "long32k":
         other_workload(args, torch, vz)
