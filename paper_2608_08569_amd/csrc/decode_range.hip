@@ -4,6 +4,8 @@
 // partial results leave the chip.
 // Compiled with the max-ILP machine scheduler (per-file flag of the build):
 // the default one over-subscribes the 256 registers per lane and spills.
+#include <atomic>
+
 #include "decode_mfma.h"
 #include "select.h"
 
@@ -49,19 +51,37 @@ constexpr int RFOLD_KEYS = 256;                    // keys per fold block; parts
 
 inline __host__ __device__ int64_t range_row(int64_t plane) { return (plane + CHUNK - 1) / CHUNK * CHUNK; }
 
-// Parts of a sequence of T keys: one part when T <= RANGE_MAX_KEYS, else the
-// fewest parts of kp keys (a multiple of RFOLD_KEYS, at most RPART), the last
-// part holding the remaining T - (P - 1) kp >= 1 keys.  (Rounding P up so
-// that the workgroups fill whole rounds of the CUs measured no faster: 2 or 4
-// parts of a 12k- or 16k-key cache took the same time.)
-__host__ __device__ inline void range_parts(int T, int& P, int& kp) {
+// Parts of a sequence of T keys in a call of `items` (layer, KV head) items
+// on `cus` compute units: one part when T <= RANGE_MAX_KEYS; else P0 =
+// ceil(T / RPART) parts at least and 2 P0 at most, P chosen to minimise
+// ceil(items P / cus) * ceil(T / P) -- whole rounds of one workgroup per CU
+// times the part length, the smallest P on ties -- so that the last round of
+// workgroups is not left to a fraction of the CUs when more, shorter parts
+// fill it (48 x 4 items at 24,576 keys: 4 parts, 3 full rounds, instead of
+// 3 parts, 2.25 rounds).  Then parts of kp keys (a multiple of RFOLD_KEYS,
+// at most RPART), the last one holding the remaining T - (P - 1) kp >= 1
+// keys.  A ragged call uses the same function, so a sequence is split the
+// same way as in a single-sequence call of the same layers and KV heads.
+__host__ __device__ inline void range_parts(int T, int items, int cus, int& P, int& kp) {
     if (T <= RANGE_MAX_KEYS) {
         P = 1;
         kp = T;
         return;
     }
     const int p0 = (T + RPART - 1) / RPART;
-    kp = ((T + p0 - 1) / p0 + RFOLD_KEYS - 1) / RFOLD_KEYS * RFOLD_KEYS;
+    int best = p0;
+    if (items > 0 && cus > 0) {
+        long long best_cost = -1;
+        for (int p = p0; p <= 2 * p0; ++p) {
+            const long long rounds = (static_cast<long long>(items) * p + cus - 1) / cus;
+            const long long cost = rounds * ((T + p - 1) / p);
+            if (best_cost < 0 || cost < best_cost) {
+                best_cost = cost;
+                best = p;
+            }
+        }
+    }
+    kp = ((T + best - 1) / best + RFOLD_KEYS - 1) / RFOLD_KEYS * RFOLD_KEYS;
     P = (T + kp - 1) / kp;
 }
 // Fold blocks of such a sequence (one per RFOLD_KEYS keys of each part).
@@ -620,11 +640,16 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     }
 }
 
-// Merge of a sequence in parts, one block per (sequence, layer) at its first
-// part: per query head the sequence's max M and sum S from the parts' pairs,
-// each part's factor exp2(m_part - M) / S (kept for the fold), and the output
-// row, the parts' outputs times their factors.
-constexpr int RMERGE_THREADS = 256;
+// Merge of a sequence in parts, one block per (sequence at its first part,
+// layer, pair of query heads): thread t takes channel t % D of head
+// 2 hb + t / D.  Per head, the sequence's max M and sum S from the parts'
+// pairs, each part's factor exp2(m_part - M) / S (kept for the fold), and the
+// output row, the parts' outputs times their factors, added in part order.
+// (Every thread of a head forms M, S and the factors itself, from the same
+// few pairs; a block per (sequence, layer) over all heads left the call's
+// merge on 48 CUs at a time.)
+constexpr int RMERGE_THREADS = 2 * D;
+constexpr int RMERGE_HEADS = RMERGE_THREADS / D;
 template <int NW, bool RAG>
 __global__ __launch_bounds__(RMERGE_THREADS) void range_merge_kernel(const FusedArgs a) {
     const int r = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
@@ -638,30 +663,26 @@ __global__ __launch_bounds__(RMERGE_THREADS) void range_merge_kernel(const Fused
     }
     if (it.P == 1 || it.p != 0) return;
     const int Hq = a.Hq, G = Hq / NW, P = it.P;
-    for (int h = t; h < Hq; h += RMERGE_THREADS) {
-        const int g = h / G, hg = h - g * G;
-        const float2* ps = rws.pstat + ((static_cast<size_t>(l) * NW + g) * a.R + r) * GMAX + hg;
-        float M = -INFINITY;
-        for (int p = 0; p < P; ++p) M = fmaxf(M, ps[static_cast<size_t>(p) * GMAX].x);
-        float S = 0.f;
-        for (int p = 0; p < P; ++p) {
-            const float2 x = ps[static_cast<size_t>(p) * GMAX];
-            S = fmaf(x.y, exp2f(x.x - M), S);
-        }
-        const float inv_S = 1.0f / S;
-        for (int p = 0; p < P; ++p)
-            rws.ftab[(static_cast<size_t>(l) * a.R + r + p) * Hq + h] = exp2f(ps[static_cast<size_t>(p) * GMAX].x - M) * inv_S;
+    const int h = static_cast<int>(blockIdx.z) * RMERGE_HEADS + t / D, ch = t % D;
+    if (h >= Hq) return;
+    const int g = h / G, hg = h - g * G;
+    const float2* ps = rws.pstat + ((static_cast<size_t>(l) * NW + g) * a.R + r) * GMAX + hg;
+    float M = -INFINITY;
+    for (int p = 0; p < P; ++p) M = fmaxf(M, ps[static_cast<size_t>(p) * GMAX].x);
+    float S = 0.f;
+    for (int p = 0; p < P; ++p) {
+        const float2 x = ps[static_cast<size_t>(p) * GMAX];
+        S = fmaf(x.y, exp2f(x.x - M), S);
     }
-    __syncthreads();  // the block's factors are visible to the block
-    for (int e = t; e < Hq * D; e += RMERGE_THREADS) {
-        const int h = e / D, ch = e - h * D;
-        const int g = h / G, hg = h - g * G;
-        const float* po = rws.pout + (((static_cast<size_t>(l) * NW + g) * a.R + r) * GMAX + hg) * D + ch;
-        const float* f = rws.ftab + (static_cast<size_t>(l) * a.R + r) * Hq + h;
-        float o = 0.f;
-        for (int p = 0; p < P; ++p) o = fmaf(po[static_cast<size_t>(p) * GMAX * D], f[static_cast<size_t>(p) * Hq], o);
-        a.out[((static_cast<size_t>(it.s) * a.L + l) * Hq + h) * D + ch] = vz::f32_to_bf16(o);
+    const float inv_S = 1.0f / S;
+    const float* po = rws.pout + (((static_cast<size_t>(l) * NW + g) * a.R + r) * GMAX + hg) * D + ch;
+    float o = 0.f;
+    for (int p = 0; p < P; ++p) {
+        const float f = exp2f(ps[static_cast<size_t>(p) * GMAX].x - M) * inv_S;
+        if (ch == 0) rws.ftab[(static_cast<size_t>(l) * a.R + r + p) * Hq + h] = f;
+        o = fmaf(po[static_cast<size_t>(p) * GMAX * D], f, o);
     }
+    a.out[((static_cast<size_t>(it.s) * a.L + l) * Hq + h) * D + ch] = vz::f32_to_bf16(o);
 }
 
 // Fold kernel of a ragged call or of a sequence in parts, one block of
@@ -736,12 +757,13 @@ __global__ __launch_bounds__(RFOLD_KEYS) void range_fold_parts_kernel(const Fuse
 constexpr int ORDER_THREADS = RANGE_MAX_SEQS;
 
 // Parts and fold blocks of sequence s (0 when it cannot be served).
+template <int NW>
 __device__ __forceinline__ void order_seq(const FusedArgs& a, int s, int& st, int& T, int& P, int& kp, int& F) {
     T = P = kp = F = 0;
     st = vz::ragged_decode_status(a.rag, s);
     if (st == VZ_OK) {
         T = a.rag.len[s] + 1;
-        range_parts(T, P, kp);
+        range_parts(T, a.L * NW, a.cus, P, kp);
         F = range_fold_blocks(T, P, kp);
     }
 }
@@ -775,7 +797,7 @@ __device__ void order_in_sequence_order(const FusedArgs& a, const RangeWs& rws, 
     int sumP = 0, sumF = 0;
     for (int s = s0; s < s1; ++s) {
         int st, T, P, kp, F;
-        order_seq(a, s, st, T, P, kp, F);
+        order_seq<NW>(a, s, st, T, P, kp, F);
         sumP += P;
         sumF += F;
     }
@@ -793,7 +815,7 @@ __device__ void order_in_sequence_order(const FusedArgs& a, const RangeWs& rws, 
     int r = s_a[t] - sumP, fb = s_b[t] - sumF;
     for (int s = s0; s < s1; ++s) {
         int st, T, P, kp, F;
-        order_seq(a, s, st, T, P, kp, F);
+        order_seq<NW>(a, s, st, T, P, kp, F);
         const bool fits = P > 0 && r + P <= a.R && fb + F <= a.FB;
         if (P > 0 && !fits) st = VZ_ERR_CAPACITY;
         if (a.rag.status) a.rag.status[s] = st;
@@ -827,7 +849,7 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
     }
     int st = VZ_OK, T = 0, P = 0, kp = 0, F = 0;
     if (t < n) {
-        order_seq(a, t, st, T, P, kp, F);
+        order_seq<NW>(a, t, st, T, P, kp, F);
         s_kp[t] = kp;
         s_P[t] = P;
         s_F[t] = F;
@@ -881,10 +903,29 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
 }
 
 // Item and fold-block bounds of a ragged call over `total` slots: a sequence
-// of T keys has at most T / RPART + 1 parts and T / RFOLD_KEYS + (parts) fold
-// blocks, and the sequences' keys add up to at most `total`.
+// of T keys has at most 2 (T / RPART + 1) parts and T / RFOLD_KEYS + (parts)
+// fold blocks, and the sequences' keys add up to at most `total`.
 int32_t ragged_items_bound(int32_t n_seqs, int64_t total) {
-    return static_cast<int32_t>(n_seqs + (total + RPART - 1) / RPART);
+    return static_cast<int32_t>(2 * (n_seqs + (total + RPART - 1) / RPART));
+}
+// Parts a single-sequence workspace holds for planes of `plane` slots.
+int32_t single_parts_bound(int64_t plane) {
+    const int64_t p0 = (plane + RPART - 1) / RPART;
+    return static_cast<int32_t>(plane > RANGE_MAX_KEYS ? 2 * p0 : p0);
+}
+// Compute units of the current device (queried once per device).
+int32_t device_cus() {
+    static std::atomic<int32_t> cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int32_t n = cus[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        n = v;
+        cus[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
 }
 int32_t ragged_fold_bound(int32_t n_seqs, int64_t total) {
     return static_cast<int32_t>((total + RFOLD_KEYS - 1) / RFOLD_KEYS + ragged_items_bound(n_seqs, total));
@@ -895,14 +936,16 @@ hipError_t launch_range(const FusedArgs& a, hipStream_t stream) {
     if (a.rag.n > 0) {
         hipLaunchKernelGGL((range_order_kernel<NW>), dim3(1), dim3(ORDER_THREADS), 0, stream, a);
         hipLaunchKernelGGL((decode_range_kernel<NW, true, true>), dim3(NW * a.L * a.R), dim3(64 * RW), 0, stream, a);
-        hipLaunchKernelGGL((range_merge_kernel<NW, true>), dim3(a.R, a.L), dim3(RMERGE_THREADS), 0, stream, a);
+        hipLaunchKernelGGL((range_merge_kernel<NW, true>), dim3(a.R, a.L, (a.Hq + RMERGE_HEADS - 1) / RMERGE_HEADS),
+                           dim3(RMERGE_THREADS), 0, stream, a);
         hipLaunchKernelGGL((range_fold_parts_kernel<NW, true>), dim3(a.FB, a.L), dim3(RFOLD_KEYS), 0, stream, a);
         return hipGetLastError();
     }
     if (a.n_parts > 1) {
         hipLaunchKernelGGL((decode_range_kernel<NW, false, true>), dim3(NW * a.L * a.n_parts), dim3(64 * RW), 0,
                            stream, a);
-        hipLaunchKernelGGL((range_merge_kernel<NW, false>), dim3(1, a.L), dim3(RMERGE_THREADS), 0, stream, a);
+        hipLaunchKernelGGL((range_merge_kernel<NW, false>), dim3(1, a.L, (a.Hq + RMERGE_HEADS - 1) / RMERGE_HEADS),
+                           dim3(RMERGE_THREADS), 0, stream, a);
         hipLaunchKernelGGL((range_fold_parts_kernel<NW, false>),
                            dim3(range_fold_blocks(a.len + 1, a.n_parts, a.part_keys), a.L), dim3(RFOLD_KEYS), 0,
                            stream, a);
@@ -921,11 +964,12 @@ bool vz_decode_range_ok(int32_t L, int32_t Hkv, int32_t n_seqs) {
 
 hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, hipStream_t stream) {
     FusedArgs a = a0;
+    a.cus = device_cus();
     if (a.rag.n > 0) {
         a.R = ragged_items_bound(a.rag.n, a.plane);
         a.FB = ragged_fold_bound(a.rag.n, a.plane);
     } else {
-        range_parts(a.len + 1, a.n_parts, a.part_keys);
+        range_parts(a.len + 1, a.L * Hkv, a.cus, a.n_parts, a.part_keys);
         a.R = a.n_parts;
         a.FB = 0;
     }
@@ -943,7 +987,7 @@ bool vz_decode_range_whole(int32_t len) { return static_cast<int64_t>(len) + 1 <
 size_t vz_decode_range_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int64_t plane, int32_t n_seqs) {
     size_t off[7];
     const bool rag = n_seqs > 0;
-    const int R = rag ? ragged_items_bound(n_seqs, plane) : static_cast<int>((plane + RPART - 1) / RPART);
+    const int R = rag ? ragged_items_bound(n_seqs, plane) : single_parts_bound(plane);
     const int FB = rag ? ragged_fold_bound(n_seqs, plane) : 0;
     return range_layout(vz_decode_hdr_bytes(L), L, Hkv, Hq, plane, R, FB, rag, off);
 }

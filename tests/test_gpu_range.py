@@ -72,8 +72,10 @@ def test_whole_range_long_sampled_layers(length):
 @pytest.mark.parametrize("length", [8224, 9215, 12000, 16384, 20000])
 def test_whole_range_parts_sampled_layers(length):
     """Caches in parts: 8225 keys (the first past one part: 2 parts of 4352
-    and 3873 keys), 12001 (2 parts), 16385 and 20001 (3 parts), two steps
-    (the second one key longer); layers 0, 13 and 31."""
+    and 3873 keys), 12001, 16385 and 20001 (2 to 6 parts: at least
+    ceil(T / 8192), more when they fill the last round of workgroups on the
+    device's CUs), two steps (the second one key longer); layers 0, 13 and
+    31."""
     run_case(32, 4, 32, length, steps=2, layers=[0, 13, 31])
 
 

@@ -153,9 +153,10 @@ def test_ragged_range_gamma_edges():
 def test_ragged_range_skips_invalid_and_overflowing_sequences():
     """A sequence with no free slot, one outside the planes and an idle slot
     are skipped (status says why, nothing of theirs written); two sequences over the
-    same 20000 slots (3 parts each) need more parts than the table holds
-    (2 sequences + 3 = 5): the first in the order (the smaller index, as the
-    parts are alike) is served, the other reported."""
+    same 20000 slots need more fold blocks than the table holds (the tables
+    are sized for sequences that do not overlap): the first in the order
+    (the smaller index, as the parts are alike) is served, the other
+    reported."""
     t = torch()
     import paper_2608_08569_amd as vz
     L, Hq, Hkv = 32, 32, 4
@@ -195,7 +196,7 @@ def test_ragged_range_skips_invalid_and_overflowing_sequences():
     check_rel(S1[[0, 31]][:, sl][:, :400], ref_s, RTOL[DT], "score")
     del K, V, Kd, Vd
 
-    # two sequences over the same slots: 20001 keys each, 3 parts each
+    # two sequences over the same slots: 20001 keys each
     total = 20010
     cap = 20005
     lens = np.array([20000, 20000])
