@@ -92,6 +92,7 @@ struct FusedArgs {
     // every key; else parts of part_keys keys, the last one shorter), and the
     // bounds of a ragged call's work tables (R parts, FB fold blocks)
     int32_t n_parts, part_keys, R, FB;
+    int32_t MB;   // a ragged call's bound on sequences in several parts
     int32_t cus;  // compute units of the device (the choice of parts)
     // whole-range path, a single sequence in one part: the last workgroup of
     // each layer to finish (elected on the arrival counters cnt[L] with the

@@ -53,12 +53,14 @@ inline __host__ __device__ int64_t range_row(int64_t plane) { return (plane + CH
 
 // Parts of a sequence of T keys in a call of `items` (layer, KV head) items
 // on `cus` compute units: one part when T <= RANGE_MAX_KEYS; else P0 =
-// ceil(T / RPART) parts at least and 2 P0 at most, P chosen to minimise
+// ceil(T / RPART) parts, or, when P0 >= 3, P0 + 1 if that makes
 // ceil(items P / cus) * ceil(T / P) -- whole rounds of one workgroup per CU
-// times the part length, the smallest P on ties -- so that the last round of
-// workgroups is not left to a fraction of the CUs when more, shorter parts
-// fill it (48 x 4 items at 24,576 keys: 4 parts, 3 full rounds, instead of
-// 3 parts, 2.25 rounds).  Then parts of kp keys (a multiple of RFOLD_KEYS,
+// times the part length -- smaller, so that the last round of workgroups is
+// not left to a fraction of the CUs (48 x 4 items at 24,576 keys: 4 parts,
+// 3 full rounds, instead of 3 parts, 2.25 rounds; with 2 parts the model
+// never prefers 3).  At most one part more, and only past 2 RPART keys,
+// keeps a ragged call's work table small: its empty workgroups cost launch
+// slots.  Then parts of kp keys (a multiple of RFOLD_KEYS,
 // at most RPART), the last one holding the remaining T - (P - 1) kp >= 1
 // keys.  A ragged call uses the same function, so a sequence is split the
 // same way as in a single-sequence call of the same layers and KV heads.
@@ -70,9 +72,9 @@ __host__ __device__ inline void range_parts(int T, int items, int cus, int& P, i
     }
     const int p0 = (T + RPART - 1) / RPART;
     int best = p0;
-    if (items > 0 && cus > 0) {
+    if (p0 >= 3 && items > 0 && cus > 0) {
         long long best_cost = -1;
-        for (int p = p0; p <= 2 * p0; ++p) {
+        for (int p = p0; p <= p0 + 1; ++p) {
             const long long rounds = (static_cast<long long>(items) * p + cus - 1) / cus;
             const long long cost = rounds * ((T + p - 1) / p);
             if (best_cost < 0 || cost < best_cost) {
@@ -110,9 +112,12 @@ static_assert(sizeof(RangeItem) == 64, "one 64-byte record per item");
 //   ftab  [L][R][Hq] float             exp2(m_part - M) / S per part and head
 //   items [R] RangeItem                a ragged call's parts, in dispatch order
 //   fblk  [FB] int2                    a ragged call's fold blocks: (item, first key)
+//   mlist [MB] int32                   a ragged call's sequences in several parts:
+//                                      the item of each one's first part
 // The parts' arrays exist when a sequence can have several parts (planes of
 // more than RANGE_MAX_KEYS slots), the tables in ragged calls only.  A ragged
-// call keeps its table sizes (items, fold blocks) in the header.
+// call keeps its table sizes (items, fold blocks, sequences in parts) in the
+// header.
 struct RangeWs {
     float* sums;
     uint16_t* rows;
@@ -121,13 +126,14 @@ struct RangeWs {
     float* ftab;
     RangeItem* items;
     int2* fblk;
-    int32_t* counts;  // [2] in the header: items, fold blocks
+    int32_t* mlist;
+    int32_t* counts;  // [3] in the header: items, fold blocks, sequences in parts
     int64_t row;
 };
 __host__ __device__ inline size_t ws_align(size_t x) { return (x + 255) / 256 * 256; }
 // Byte offsets of the arrays from the start of the workspace; returns the end.
 __host__ __device__ inline size_t range_layout(size_t hdr, int L, int NW, int Hq, int64_t plane, int R, int FB,
-                                               bool ragged, size_t off[7]) {
+                                               int MB, bool ragged, size_t off[8]) {
     const size_t row = static_cast<size_t>(range_row(plane));
     const size_t heads = static_cast<size_t>(L) * NW;
     const bool parts = plane > RANGE_MAX_KEYS;
@@ -146,12 +152,14 @@ __host__ __device__ inline size_t range_layout(size_t hdr, int L, int NW, int Hq
     if (ragged) o = ws_align(o + static_cast<size_t>(R) * sizeof(RangeItem));
     off[6] = o;
     if (ragged) o = ws_align(o + static_cast<size_t>(FB) * sizeof(int2));
+    off[7] = o;
+    if (ragged) o = ws_align(o + static_cast<size_t>(MB) * sizeof(int32_t));
     return o;
 }
 template <int NW>
 __device__ __forceinline__ RangeWs range_ws(const FusedArgs& a, bool ragged) {
-    size_t off[7];
-    range_layout(a.hdr_bytes, a.L, NW, a.Hq, a.plane, a.R, a.FB, ragged, off);
+    size_t off[8];
+    range_layout(a.hdr_bytes, a.L, NW, a.Hq, a.plane, a.R, a.FB, a.MB, ragged, off);
     RangeWs w;
     w.sums = reinterpret_cast<float*>(a.ws + off[0]);
     w.rows = reinterpret_cast<uint16_t*>(a.ws + off[1]);
@@ -160,6 +168,7 @@ __device__ __forceinline__ RangeWs range_ws(const FusedArgs& a, bool ragged) {
     w.ftab = reinterpret_cast<float*>(a.ws + off[4]);
     w.items = reinterpret_cast<RangeItem*>(a.ws + off[5]);
     w.fblk = reinterpret_cast<int2*>(a.ws + off[6]);
+    w.mlist = reinterpret_cast<int32_t*>(a.ws + off[7]);
     w.counts = reinterpret_cast<int32_t*>(a.ws);
     w.row = range_row(a.plane);
     return w;
@@ -640,9 +649,10 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     }
 }
 
-// Merge of a sequence in parts, one block per (sequence at its first part,
-// layer, pair of query heads): thread t takes channel t % D of head
-// 2 hb + t / D.  Per head, the sequence's max M and sum S from the parts'
+// Merge of a sequence in parts, one block per (sequence in parts, layer,
+// pair of query heads) -- a ragged call's sequences in parts are listed by
+// the order kernel, a single sequence is item 0 -- and thread t takes
+// channel t % D of head 2 hb + t / D.  Per head, the sequence's max M and sum S from the parts'
 // pairs, each part's factor exp2(m_part - M) / S (kept for the fold), and the
 // output row, the parts' outputs times their factors, added in part order.
 // (Every thread of a head forms M, S and the factors itself, from the same
@@ -652,11 +662,13 @@ constexpr int RMERGE_THREADS = 2 * D;
 constexpr int RMERGE_HEADS = RMERGE_THREADS / D;
 template <int NW, bool RAG>
 __global__ __launch_bounds__(RMERGE_THREADS) void range_merge_kernel(const FusedArgs a) {
-    const int r = blockIdx.x, l = blockIdx.y, t = threadIdx.x;
+    const int l = blockIdx.y, t = threadIdx.x;
     const RangeWs rws = range_ws<NW>(a, RAG);
+    int r = 0;
     RangeItem it;
     if constexpr (RAG) {
-        if (r >= rws.counts[0]) return;
+        if (static_cast<int>(blockIdx.x) >= rws.counts[2]) return;
+        r = rws.mlist[blockIdx.x];
         it = rws.items[r];
     } else {
         it = single_item(a, r);
@@ -790,42 +802,49 @@ __device__ void order_write(const FusedArgs& a, const RangeWs& rws, int s, int T
 }
 
 template <int NW>
-__device__ void order_in_sequence_order(const FusedArgs& a, const RangeWs& rws, int* s_a, int* s_b, int* s_n) {
+__device__ void order_in_sequence_order(const FusedArgs& a, const RangeWs& rws, int* s_a, int* s_b, int* s_c,
+                                        int* s_n) {
     const int n = a.rag.n, t = threadIdx.x;
     const int per = (n + ORDER_THREADS - 1) / ORDER_THREADS;
     const int s0 = min(t * per, n), s1 = min(s0 + per, n);
-    int sumP = 0, sumF = 0;
+    int sumP = 0, sumF = 0, sumM = 0;
     for (int s = s0; s < s1; ++s) {
         int st, T, P, kp, F;
         order_seq<NW>(a, s, st, T, P, kp, F);
         sumP += P;
         sumF += F;
+        sumM += P > 1;
     }
-    // exclusive block scan of the runs' items and fold blocks
+    // exclusive block scan of the runs' items, fold blocks and sequences in parts
     s_a[t] = sumP;
     s_b[t] = sumF;
+    s_c[t] = sumM;
     __syncthreads();
     for (int o = 1; o < ORDER_THREADS; o <<= 1) {
-        const int xa = t >= o ? s_a[t - o] : 0, xb = t >= o ? s_b[t - o] : 0;
+        const int xa = t >= o ? s_a[t - o] : 0, xb = t >= o ? s_b[t - o] : 0, xc = t >= o ? s_c[t - o] : 0;
         __syncthreads();
         s_a[t] += xa;
         s_b[t] += xb;
+        s_c[t] += xc;
         __syncthreads();
     }
-    int r = s_a[t] - sumP, fb = s_b[t] - sumF;
+    int r = s_a[t] - sumP, fb = s_b[t] - sumF, m = s_c[t] - sumM;
     for (int s = s0; s < s1; ++s) {
         int st, T, P, kp, F;
         order_seq<NW>(a, s, st, T, P, kp, F);
-        const bool fits = P > 0 && r + P <= a.R && fb + F <= a.FB;
+        const bool fits = P > 0 && r + P <= a.R && fb + F <= a.FB && m + (P > 1) <= a.MB;
         if (P > 0 && !fits) st = VZ_ERR_CAPACITY;
         if (a.rag.status) a.rag.status[s] = st;
         if (fits) {
             order_write(a, rws, s, T, P, kp, r, fb, true);
+            if (P > 1) rws.mlist[m] = r;
             atomicMax(&s_n[1], r + P);
             atomicMax(&s_n[2], fb + F);
+            atomicMax(&s_n[3], m + (P > 1));
         }
         r += P;
         fb += F;
+        m += P > 1;
     }
 }
 
@@ -833,17 +852,18 @@ template <int NW>
 __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedArgs a) {
     __shared__ int s_kp[ORDER_THREADS], s_P[ORDER_THREADS], s_F[ORDER_THREADS];
     __shared__ int s_seq[ORDER_THREADS], s_fb[ORDER_THREADS], s_r0[ORDER_THREADS];
-    __shared__ int s_n[3];  // sequences served, items, fold blocks
+    __shared__ int s_n[4];  // sequences served, items, fold blocks, sequences in parts
     const RangeWs rws = range_ws<NW>(a, true);
     const int n = a.rag.n, t = threadIdx.x;
-    if (t < 3) s_n[t] = 0;
+    if (t < 4) s_n[t] = 0;
     if (n > ORDER_THREADS) {
         __syncthreads();
-        order_in_sequence_order<NW>(a, rws, s_kp, s_P, s_n);
+        order_in_sequence_order<NW>(a, rws, s_kp, s_P, s_F, s_n);
         __syncthreads();
         if (t == 0) {
             rws.counts[0] = s_n[1];
             rws.counts[1] = s_n[2];
+            rws.counts[2] = s_n[3];
         }
         return;
     }
@@ -855,8 +875,9 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
         s_F[t] = F;
     }
     __syncthreads();
-    // position among the served sequences, first item, first fold block
-    int q = 0, r0 = 0, fb0 = 0;
+    // position among the served sequences, first item, first fold block,
+    // sequences in parts before it
+    int q = 0, r0 = 0, fb0 = 0, m0 = 0;
     if (P > 0) {
         for (int u = 0; u < n; ++u) {
             const int ku = s_kp[u];
@@ -864,12 +885,13 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
                 ++q;
                 r0 += s_P[u];
                 fb0 += s_F[u];
+                m0 += s_P[u] > 1;
             }
         }
     }
     // a sequence that does not fit pushes every later one out as well, so the
     // served ones hold positions 0 .. served - 1
-    const bool fits = P > 0 && r0 + P <= a.R && fb0 + F <= a.FB;
+    const bool fits = P > 0 && r0 + P <= a.R && fb0 + F <= a.FB && m0 + (P > 1) <= a.MB;
     if (P > 0 && !fits) st = VZ_ERR_CAPACITY;
     if (t < n && a.rag.status) a.rag.status[t] = st;
     if (fits) {
@@ -879,6 +901,8 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
         atomicAdd(&s_n[0], 1);
         atomicMax(&s_n[1], r0 + P);
         atomicMax(&s_n[2], fb0 + F);
+        atomicMax(&s_n[3], m0 + (P > 1));
+        if (P > 1) rws.mlist[m0] = r0;
         order_write(a, rws, t, T, P, kp, r0, fb0, false);  // fold entries below, spread over the block
     }
     __syncthreads();
@@ -899,19 +923,22 @@ __global__ __launch_bounds__(ORDER_THREADS) void range_order_kernel(const FusedA
     if (t == 0) {
         rws.counts[0] = s_n[1];
         rws.counts[1] = n_fold;
+        rws.counts[2] = s_n[3];
     }
 }
 
 // Item and fold-block bounds of a ragged call over `total` slots: a sequence
-// of T keys has at most 2 (T / RPART + 1) parts and T / RFOLD_KEYS + (parts)
-// fold blocks, and the sequences' keys add up to at most `total`.
+// of T keys has at most ceil(T / RPART) parts, one more past 2 RPART keys,
+// and T / RFOLD_KEYS + (parts) fold blocks; the sequences' keys add up to at
+// most `total`, so at most total / (2 RPART + 1) of them are that long.
 int32_t ragged_items_bound(int32_t n_seqs, int64_t total) {
-    return static_cast<int32_t>(2 * (n_seqs + (total + RPART - 1) / RPART));
+    const int64_t longs = total / (2 * RPART + 1);
+    return static_cast<int32_t>(n_seqs + (total + RPART - 1) / RPART + (longs < n_seqs ? longs : n_seqs));
 }
 // Parts a single-sequence workspace holds for planes of `plane` slots.
 int32_t single_parts_bound(int64_t plane) {
     const int64_t p0 = (plane + RPART - 1) / RPART;
-    return static_cast<int32_t>(plane > RANGE_MAX_KEYS ? 2 * p0 : p0);
+    return static_cast<int32_t>(p0 >= 3 ? p0 + 1 : p0);
 }
 // Compute units of the current device (queried once per device).
 int32_t device_cus() {
@@ -927,6 +954,12 @@ int32_t device_cus() {
     }
     return n;
 }
+// Sequences of a ragged call that can be in several parts: more than
+// RANGE_MAX_KEYS keys each, in non-overlapping slots of `total`.
+int32_t ragged_multi_bound(int32_t n_seqs, int64_t total) {
+    const int64_t longs = total / (RANGE_MAX_KEYS + 1);
+    return static_cast<int32_t>(longs < n_seqs ? longs : n_seqs);
+}
 int32_t ragged_fold_bound(int32_t n_seqs, int64_t total) {
     return static_cast<int32_t>((total + RFOLD_KEYS - 1) / RFOLD_KEYS + ragged_items_bound(n_seqs, total));
 }
@@ -936,8 +969,10 @@ hipError_t launch_range(const FusedArgs& a, hipStream_t stream) {
     if (a.rag.n > 0) {
         hipLaunchKernelGGL((range_order_kernel<NW>), dim3(1), dim3(ORDER_THREADS), 0, stream, a);
         hipLaunchKernelGGL((decode_range_kernel<NW, true, true>), dim3(NW * a.L * a.R), dim3(64 * RW), 0, stream, a);
-        hipLaunchKernelGGL((range_merge_kernel<NW, true>), dim3(a.R, a.L, (a.Hq + RMERGE_HEADS - 1) / RMERGE_HEADS),
-                           dim3(RMERGE_THREADS), 0, stream, a);
+        if (a.MB > 0)
+            hipLaunchKernelGGL((range_merge_kernel<NW, true>),
+                               dim3(a.MB, a.L, (a.Hq + RMERGE_HEADS - 1) / RMERGE_HEADS), dim3(RMERGE_THREADS), 0,
+                               stream, a);
         hipLaunchKernelGGL((range_fold_parts_kernel<NW, true>), dim3(a.FB, a.L), dim3(RFOLD_KEYS), 0, stream, a);
         return hipGetLastError();
     }
@@ -968,6 +1003,7 @@ hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, hipStream_t 
     if (a.rag.n > 0) {
         a.R = ragged_items_bound(a.rag.n, a.plane);
         a.FB = ragged_fold_bound(a.rag.n, a.plane);
+        a.MB = ragged_multi_bound(a.rag.n, a.plane);
     } else {
         range_parts(a.len + 1, a.L * Hkv, a.cus, a.n_parts, a.part_keys);
         a.R = a.n_parts;
@@ -985,10 +1021,11 @@ hipError_t vz_launch_decode_range(const FusedArgs& a0, int32_t Hkv, hipStream_t 
 bool vz_decode_range_whole(int32_t len) { return static_cast<int64_t>(len) + 1 <= RANGE_MAX_KEYS; }
 
 size_t vz_decode_range_ws_bytes(int32_t L, int32_t Hq, int32_t Hkv, int64_t plane, int32_t n_seqs) {
-    size_t off[7];
+    size_t off[8];
     const bool rag = n_seqs > 0;
     const int R = rag ? ragged_items_bound(n_seqs, plane) : single_parts_bound(plane);
     const int FB = rag ? ragged_fold_bound(n_seqs, plane) : 0;
-    return range_layout(vz_decode_hdr_bytes(L), L, Hkv, Hq, plane, R, FB, rag, off);
+    const int MB = rag ? ragged_multi_bound(n_seqs, plane) : 0;
+    return range_layout(vz_decode_hdr_bytes(L), L, Hkv, Hq, plane, R, FB, MB, rag, off);
 }
 
