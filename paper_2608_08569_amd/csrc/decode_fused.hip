@@ -215,8 +215,13 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
     }
 
     // both tiles requested at once; rows past the chunk read as zero without
-    // touching memory (bounded scalar descriptors)
+    // touching memory (bounded scalar descriptors).  The V tile comes whole
+    // rows at a time (instruction m: rows 4 m .. 4 m + 3) for its trip through
+    // LDS; the K tile straight in the MFMA A-operand layout (register m =
+    // 4 ti + s: row 16 ti + r16, bytes 16 (q4 + 4 s) .. + 15), used from
+    // registers.
     const int lane_off = q4 * (D * 2) + 16 * r16;
+    const int lane_off_k = r16 * (D * 2) + 16 * q4;
     uint4 kt[8], vt[8];
     {
         const __amdgpu_buffer_rsrc_t rk =
@@ -225,7 +230,8 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
             __builtin_amdgcn_make_buffer_rsrc(Vh + static_cast<size_t>(kw0) * D, 0, rows * D * 2, kBufferDword3);
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
-            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off + 4 * m * (D * 2), 0, 0);
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off_k + (m >> 2) * 16 * (D * 2) + (m & 3) * 64,
+                                                                 0, 0);
             __builtin_memcpy(&kt[m], &v, 16);
         }
 #pragma unroll
@@ -245,24 +251,18 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
         }
     }
     uint8_t* const buf = s_tile[w];
-    uint8_t* const kwp = buf + q4 * KSTRIDE + 16 * r16;
     uint8_t* const vwp = buf + q4 * VSTRIDE + 16 * r16;
-    const uint8_t* const kr = buf + r16 * KSTRIDE + 16 * q4;
     const uint8_t* const vr = buf + (4 * q4 + (r16 >> 2)) * VSTRIDE + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
 
     // ---- logits of the wave's 32 keys: S^T = K Q^T ----
-#pragma unroll
-    for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(kwp + 4 * KSTRIDE * m) = kt[m];
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is in LDS
     f32x4 acc[2];
 #pragma unroll
     for (int ti = 0; ti < 2; ++ti) {
         acc[ti] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < KSTEPS; ++s) {
-            const uint4 av = *reinterpret_cast<const uint4*>(kr + 16 * KSTRIDE * ti + 64 * s);
-            acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(qv[s]), acc[ti], 0, 0, 0);
-        }
+        for (int s = 0; s < KSTEPS; ++s)
+            acc[ti] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kt[4 * ti + s]), as_bf16x8(qv[s]), acc[ti], 0,
+                                                              0, 0);
     }
     float sp[4];
 #pragma unroll
@@ -277,7 +277,6 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
     m_w = fmaxf(m_w, __shfl_xor(m_w, 32, 64));
     m_w = fmaxf(m_w, ror8(m_w));
     if (q4 == 0 && hi == 0) s_m[w][hh] = m_w;
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // the K tile's reads are done: the V tile takes the buffer
 #pragma unroll
     for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vwp + 4 * VSTRIDE * m) = vt[m];
     __syncthreads();

@@ -30,7 +30,9 @@ constexpr int kBufferDword3 = 0x00020000;  // raw buffer descriptor word 3 (32-b
 // LDS address is one per-lane base plus an immediate (bank analysis in the
 // design notes): K rows 272 bytes apart (16 rows at one 16-byte column fall on
 // 16 distinct bank groups), V rows 288 bytes apart (4 rows x 32 bytes of a
-// transposed read fall on distinct banks).
+// transposed read fall on distinct banks).  (The chunked attend kernel loads
+// its K tiles straight into the MFMA operand layout instead; only its V
+// tiles go through LDS.)
 constexpr int KSTRIDE = 256 + 16;
 constexpr int VSTRIDE = 256 + 32;
 constexpr int TILE_BYTES = VT * VSTRIDE;
