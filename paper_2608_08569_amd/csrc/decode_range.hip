@@ -283,7 +283,13 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     // only when n_full = RW * RFULL, where the part limit (RANGE_MAX_KEYS keys
     // for a whole sequence, RPART for a part of a longer one) leaves it <= VT
     // keys.
-    auto chunk_of = [&](int k) { return k < my_full ? c0 + k : n_full; };
+    // Steps whose new position is odd take the full chunks of every wave in
+    // reverse order: consecutive steps of a sequence re-read the same cache,
+    // and the keys a step reads last are then the first the next step reads,
+    // while they are still in the memory-side cache (Infinity Cache).  The
+    // order follows from the call's arguments, so a step's bits do too.
+    const bool rev = (it.next_pos & 1) != 0;
+    auto chunk_of = [&](int k) { return k < my_full ? (rev ? c0 + my_full - 1 - k : c0 + k) : n_full; };
     const size_t seq_row = static_cast<size_t>(it.s) * a.L + l;  // (sequence, layer) row of q, out, k_new, v_new
     const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base + it.k0) * D;
     uint16_t* Kh = a.k_cache + head_base;  // the item's first key
