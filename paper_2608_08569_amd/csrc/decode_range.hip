@@ -275,30 +275,41 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     const int NK = it.k1 - it.k0;             // keys of this item
     const int n_full = NK / CHUNK;            // full chunks; chunk n_full holds the other NK % CHUNK keys
     const bool part = NK % CHUNK != 0;
-    const int c0 = __builtin_amdgcn_readfirstlane(w * n_full / RW);  // the wave's full chunks: [c0, c0 + my_full)
-    const int my_full = __builtin_amdgcn_readfirstlane((w + 1) * n_full / RW - c0);
+    // Steps whose new position is odd read the chunks in the other
+    // direction (see chunk_of below) and, where wave 0's last slot allows it,
+    // with the two halves of the waves' ranges exchanged: the first wave of
+    // each SIMD, which gets the memory pipe first, then starts on the range
+    // the second one read last in the previous step.
+    const bool odd = (it.next_pos & 1) != 0;
+    const int half = RW / 2;
+    const int s_half = ((half + 1) * n_full) / RW - (half * n_full) / RW;  // full chunks of range RW / 2
+    const bool swap = odd && (s_half < RFULL || NK % CHUNK <= VT);  // wave 0 keeps the partial chunk
+    const int wr = swap ? (w ^ half) : w;  // the wave's range
+    const int c0 = __builtin_amdgcn_readfirstlane(wr * n_full / RW);  // the wave's full chunks: [c0, c0 + my_full)
+    const int my_full = __builtin_amdgcn_readfirstlane((wr + 1) * n_full / RW - c0);
     const int my_chunks = my_full + (w == 0 && part ? 1 : 0);
-    // Chunk of the wave's slot k.  Wave 0 has the fewest full chunks
-    // (n_full / RW), so the partial chunk is at most its slot RFULL, and there
-    // only when n_full = RW * RFULL, where the part limit (RANGE_MAX_KEYS keys
-    // for a whole sequence, RPART for a part of a longer one) leaves it <= VT
-    // keys.
-    // Steps whose new position is odd take the full chunks of every wave in
-    // reverse order: consecutive steps of a sequence re-read the same cache,
-    // and the keys a step reads last are then the first the next step reads,
-    // while they are still in the memory-side cache (Infinity Cache).  The
-    // order follows from the call's arguments, so a step's bits do too.
-    const bool rev = (it.next_pos & 1) != 0;
-    auto chunk_of = [&](int k) { return k < my_full ? (rev ? c0 + my_full - 1 - k : c0 + k) : n_full; };
+    // Chunk of the wave's slot k.  Range 0 has the fewest full chunks
+    // (n_full / RW), so on wave 0 the partial chunk is at most its slot
+    // RFULL, and there only when n_full = RW * RFULL, where the part limit
+    // (RANGE_MAX_KEYS keys for a whole sequence, RPART for a part of a longer
+    // one) leaves it <= VT keys; with the ranges exchanged, wave 0 holds range
+    // RW / 2, which the condition on `swap` keeps to the same bound.
+    // Odd steps take the full chunks of every wave in reverse order:
+    // consecutive steps of a sequence re-read the same cache, and the keys a
+    // step reads last are then the first the next step reads, while they are
+    // still in the memory-side cache (Infinity Cache).  The order follows from
+    // the call's arguments, so a step's bits do too.
+    auto chunk_of = [&](int k) { return k < my_full ? (odd ? c0 + my_full - 1 - k : c0 + k) : n_full; };
     const size_t seq_row = static_cast<size_t>(it.s) * a.L + l;  // (sequence, layer) row of q, out, k_new, v_new
     const size_t head_base = ((static_cast<size_t>(l) * NW + g) * a.plane + it.base + it.k0) * D;
     uint16_t* Kh = a.k_cache + head_base;  // the item's first key
     uint16_t* Vh = a.v_cache + head_base;
 
     // Eq. (1) first: in the last part, the wave whose chunks hold slot len
-    // (the partial chunk's wave 0, else the last wave) writes the new row
-    // before any of its loads, so every key is read from the cache alike.
-    if (it.p == it.P - 1 && w == (part ? 0 : RW - 1)) {
+    // (the partial chunk's wave 0, else the wave holding range RW - 1) writes
+    // the new row before any of its loads, so every key is read from the
+    // cache alike.
+    if (it.p == it.P - 1 && w == (part ? 0 : (RW - 1) ^ (swap ? half : 0))) {
         const uint16_t* kn = a.k_new + (seq_row * NW + g) * D;
         const uint16_t* vn = a.v_new + (seq_row * NW + g) * D;
         const size_t at = static_cast<size_t>(len - it.k0) * D;

@@ -69,6 +69,17 @@ def test_whole_range_long_sampled_layers(length):
     run_case(32, 4, 32, length, steps=1, layers=[0, 13, 31])
 
 
+@pytest.mark.parametrize("length", [7827, 7907, 8163])
+def test_whole_range_alternating_order(length):
+    """Two steps each (the new positions of consecutive steps differ in
+    parity, so both read orders run): 7828 keys (61 full chunks and a 20-key
+    partial one: on the odd step the waves' ranges are exchanged and wave 0
+    holds 8 full chunks and the partial one in its last slot), 7908 and 8164
+    (61 and 63 full chunks with a 100-key partial chunk: reversed without
+    the exchange); layers 0, 13 and 31."""
+    run_case(32, 4, 32, length, steps=2, layers=[0, 13, 31])
+
+
 @pytest.mark.parametrize("length", [8224, 9215, 12000, 16384, 20000])
 def test_whole_range_parts_sampled_layers(length):
     """Caches in parts: 8225 keys (the first past one part: 2 parts of 4352
