@@ -261,7 +261,11 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
     constexpr bool FLAT = RAG || SPLIT;
     const int g = FLAT ? static_cast<int>(blockIdx.x) % NW : static_cast<int>(blockIdx.x);
     const int l = FLAT ? (static_cast<int>(blockIdx.x) / NW) % a.L : static_cast<int>(blockIdx.y);
-    const int r = FLAT ? static_cast<int>(blockIdx.x) / (NW * a.L) : 0;
+    // (a single sequence in parts takes them last to first on odd steps, as
+    // the waves their chunks below: the parts a step reads last, in its last
+    // round of workgroups, are then the first the next step reads)
+    const int r0 = FLAT ? static_cast<int>(blockIdx.x) / (NW * a.L) : 0;
+    const int r = !RAG && SPLIT && (a.next_pos & 1) ? a.n_parts - 1 - r0 : r0;
     const RangeWs rws = range_ws<NW>(a, RAG);
     RangeItem it;
     if constexpr (RAG) {
