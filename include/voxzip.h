@@ -42,7 +42,7 @@ extern "C" {
 #define VZ_ERR_INVALID -1     /* a null pointer, a bad scalar (gamma, budget, windows) */
 #define VZ_ERR_SHAPE -2       /* inconsistent sizes (n_q_heads % kv_heads, d, counts) */
 #define VZ_ERR_CAPACITY -3    /* the cache or an output has no room */
-#define VZ_ERR_UNSUPPORTED -4 /* dtype / head size / group size this build does not serve */
+#define VZ_ERR_UNSUPPORTED -4 /* dtype / head size / group size the library does not serve */
 #define VZ_ERR_HIP -5         /* a HIP call failed; voxzip_last_error() has its text */
 #define VZ_ERR_WORKSPACE -6   /* workspace missing, not 16-byte aligned, or smaller than voxzip_workspace_bytes() */
 #define VZ_IDLE 1             /* per-sequence status of a ragged call: an idle batch slot (cap[s] == 0), skipped */
