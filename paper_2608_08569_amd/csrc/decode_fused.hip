@@ -153,10 +153,11 @@ __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem
 // over 260 workgroups.  The waves agree on the chunk's max per head through
 // LDS, then sum their exp2 sums and partial outputs in wave order; the
 // partial results of (chunk, query head) go to the workspace for the
-// finishing kernels.
+// finishing kernels.  (Launch bounds: four workgroups per CU, 128 registers
+// per lane; the MFMA accumulators then live in ordinary vector registers.)
 constexpr int SPLIT_W = CHUNK / VT;  // waves per chunk: one 32-key tile each
 template <int NW, bool RAG>
-__global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const FusedArgs a) {
+__global__ __launch_bounds__(64 * SPLIT_W, 4) void decode_attend_kernel(const FusedArgs a) {
     constexpr int OS = D + 4;  // padded LDS row of a wave's partial output (floats)
     static_assert(SPLIT_W * GMAX * OS * 4 <= SPLIT_W * TILE_BYTES, "the partial outputs fit in the tile buffers");
     __shared__ __attribute__((aligned(16))) uint8_t s_tile[SPLIT_W][TILE_BYTES];
@@ -200,18 +201,38 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
     uint16_t* Vh = a.v_cache + head_base;
     const size_t row_sl = static_cast<size_t>(it.s) * a.L + l;
 
-    // Eq. (1) first: the wave whose keys hold slot len writes the new row of
-    // its KV head before its loads (and KV head 0 the position).
-    if (len >= kw0 && len < kw0 + VT) {
+    // Eq. (1): the wave whose keys hold slot len (row rr of its tile) loads
+    // its KV head's new K and V rows with its other loads, puts them into its
+    // tile registers in place of the cache's old row once the tiles have
+    // landed, and only then writes them to the cache (and KV head 0 the
+    // position), so that none of the chunk's loads waits behind a write.
+    // Lane (r16, q4) holds K channels 8 (q4 + 4 s) .. + 7 of its K rows and V
+    // channels 8 r16 .. + 7 of its V rows (the tile layouts below).
+    const int rr = len - kw0;
+    const bool writer = rr >= 0 && rr < VT;  // wave-uniform
+    uint4 kn_row[KSTEPS], vn_row;
+    if (writer) {
         const uint16_t* kn = a.k_new + (row_sl * NW + g) * D;
         const uint16_t* vn = a.v_new + (row_sl * NW + g) * D;
-        if (lane < 16)
-            *reinterpret_cast<uint4*>(Kh + len * D + 8 * lane) = *reinterpret_cast<const uint4*>(kn + 8 * lane);
-        else if (lane < 32)
-            *reinterpret_cast<uint4*>(Vh + len * D + 8 * (lane - 16)) =
-                *reinterpret_cast<const uint4*>(vn + 8 * (lane - 16));
-        if (g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
-        __threadfence_block();
+#pragma unroll
+        for (int s = 0; s < KSTEPS; ++s) kn_row[s] = *reinterpret_cast<const uint4*>(kn + 8 * (q4 + 4 * s));
+        vn_row = *reinterpret_cast<const uint4*>(vn + 8 * r16);
+    }
+
+    // The query rows first, so that the logits wait for them and the K tile
+    // only, not for the V tile behind them.  One descriptor over the KV
+    // head's G query rows: lanes of head columns r16 >= G read past it and
+    // get zeros, with no memory access.
+    uint4 qv[KSTEPS];
+    {
+        const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(a.q + (row_sl * Hq + g * G) * D), 0, __builtin_amdgcn_readfirstlane(G * D * 2),
+            kBufferDword3);
+#pragma unroll
+        for (int s = 0; s < KSTEPS; ++s) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rq, (r16 * D + 8 * q4 + 32 * s) * 2, 0, 0);
+            __builtin_memcpy(&qv[s], &v, 16);
+        }
     }
 
     // both tiles requested at once; rows past the chunk read as zero without
@@ -224,10 +245,14 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
     const int lane_off_k = r16 * (D * 2) + 16 * q4;
     uint4 kt[8], vt[8];
     {
+        // (the byte bound taken through readfirstlane keeps the descriptors in
+        // scalar registers: a bound left in a vector register makes the
+        // compiler wrap every load in a loop over the lanes' descriptors)
+        const int nbytes = __builtin_amdgcn_readfirstlane(rows * D * 2);
         const __amdgpu_buffer_rsrc_t rk =
-            __builtin_amdgcn_make_buffer_rsrc(Kh + static_cast<size_t>(kw0) * D, 0, rows * D * 2, kBufferDword3);
+            __builtin_amdgcn_make_buffer_rsrc(Kh + static_cast<size_t>(kw0) * D, 0, nbytes, kBufferDword3);
         const __amdgpu_buffer_rsrc_t rv =
-            __builtin_amdgcn_make_buffer_rsrc(Vh + static_cast<size_t>(kw0) * D, 0, rows * D * 2, kBufferDword3);
+            __builtin_amdgcn_make_buffer_rsrc(Vh + static_cast<size_t>(kw0) * D, 0, nbytes, kBufferDword3);
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
             const auto v = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off_k + (m >> 2) * 16 * (D * 2) + (m & 3) * 64,
@@ -240,19 +265,18 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
             __builtin_memcpy(&vt[m], &v, 16);
         }
     }
-    uint4 qv[KSTEPS];
-    {
-        const int hq = r16 < G ? r16 : 0;
-        const uint16_t* qrow = a.q + (row_sl * Hq + g * G + hq) * D + 8 * q4;
-#pragma unroll
-        for (int s = 0; s < KSTEPS; ++s) {
-            const uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * s);
-            qv[s] = (r16 < G) ? v : make_uint4(0, 0, 0, 0);
-        }
-    }
+    __builtin_amdgcn_sched_barrier(0);  // every load above is issued before the first wait
     uint8_t* const buf = s_tile[w];
     uint8_t* const vwp = buf + q4 * VSTRIDE + 16 * r16;
     const uint8_t* const vr = buf + (4 * q4 + (r16 >> 2)) * VSTRIDE + 16 * ((r16 & 3) >> 1) + 8 * (r16 & 1);
+
+    if (writer && r16 == (rr & 15)) {  // the new K row: row 16 ti + r16 of registers 4 ti .. 4 ti + 3
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti)
+            if (ti == rr >> 4)
+#pragma unroll
+                for (int s = 0; s < KSTEPS; ++s) kt[4 * ti + s] = kn_row[s];
+    }
 
     // ---- logits of the wave's 32 keys: S^T = K Q^T ----
     f32x4 acc[2];
@@ -277,6 +301,20 @@ __global__ __launch_bounds__(64 * SPLIT_W) void decode_attend_kernel(const Fused
     m_w = fmaxf(m_w, __shfl_xor(m_w, 32, 64));
     m_w = fmaxf(m_w, ror8(m_w));
     if (q4 == 0 && hi == 0) s_m[w][hh] = m_w;
+    if (writer) {
+        if (q4 == (rr & 3)) {  // the new V row: row 4 m + q4 of register m
+#pragma unroll
+            for (int m = 0; m < 8; ++m)
+                if (m == rr >> 2) vt[m] = vn_row;
+        }
+        // the new rows into the cache, after every load of the wave
+        if (r16 == (rr & 15)) {
+#pragma unroll
+            for (int s = 0; s < KSTEPS; ++s) *reinterpret_cast<uint4*>(Kh + len * D + 8 * (q4 + 4 * s)) = kn_row[s];
+        }
+        if (q4 == (rr & 3)) *reinterpret_cast<uint4*>(Vh + len * D + 8 * r16) = vn_row;
+        if (g == 0 && lane == 0) a.pos[static_cast<size_t>(l) * a.plane + it.base + len] = it.next_pos;
+    }
 #pragma unroll
     for (int m = 0; m < 8; ++m) *reinterpret_cast<uint4*>(vwp + 4 * VSTRIDE * m) = vt[m];
     __syncthreads();

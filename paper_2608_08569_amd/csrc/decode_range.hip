@@ -339,8 +339,10 @@ __global__ __launch_bounds__(64 * RW, 1) void decode_range_kernel(const FusedArg
         const int u = j & 3;
         const int rows = nk - VT * u > 0 ? nk - VT * u : 0;
         const uint16_t* base = (j < 4 ? Kh : Vh) + (static_cast<size_t>(c) * CHUNK + VT * u) * D;
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, rows * D * 2, kBufferDword3);
+        // (the byte bound through readfirstlane: in a vector register it would
+        // make the compiler wrap each load in a loop over the lanes' descriptors)
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(base), 0, __builtin_amdgcn_readfirstlane(rows * D * 2), kBufferDword3);
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
             const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, lane_off + 4 * m * (D * 2), 0, 0);
