@@ -683,6 +683,7 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
     };
     SeqItem it;
     int c;
+    float a_spec = 0.f;
     if (one) {
         // the sequence's values first (a ragged call of one: sequence 0 owns
         // chunk rows [0, its chunks)), then the partial results, then the
@@ -697,6 +698,11 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
         }
         load_pairs(static_cast<size_t>(l) * a.nc_max, RAG ? a.nc_max : a.n_chunks);
         load_own((static_cast<size_t>(l) * a.nc_max + blockIdx.x) * Hq);
+        // the score of key tk of chunk blockIdx.x for a sequence at slot 0
+        // (a single-sequence call, or the one slot of a decode loop), with the
+        // other loads; another base loads it again once the values are in
+        a_spec = a.score[static_cast<size_t>(l) * a.plane +
+                         min(static_cast<int64_t>(chunk_begin(blockIdx.x) + tk), a.plane - 1)];
         int nc = a.n_chunks;
         if constexpr (RAG) {
             const bool ok = vz::decode_status_of(b, cp, ln, np, a.rag.total) == VZ_OK;
@@ -725,7 +731,8 @@ __global__ __launch_bounds__(OUT_THREADS) void decode_finish_kernel(const FusedA
     const int nk = chunk_keys(c, T);
     const int j = chunk_begin(c) + (tk < nk ? tk : 0);
     float* sc = a.score + static_cast<size_t>(l) * a.plane + it.base + j;
-    const float a_ld = *sc;
+    // (used only for tk < nk, where j is the slot the speculative load read)
+    const float a_ld = one && it.base == 0 ? a_spec : *sc;
     const uint16_t* pp = part.p + cbase * CHUNK + tk;
 
     // the layer statistics of every head: row group rg of head h takes
