@@ -8,13 +8,14 @@
 // (decode_range.hip) instead.
 //
 // Attend kernel: work item = (layer, key chunk of <= 128 keys, KV head), a
-// workgroup of four waves, one 32-key tile each (the K and V tiles of a wave
-// are requested at once: one memory round trip per chunk).
+// workgroup of four waves, one 32-key tile each (the query rows and the K
+// and V tiles of a wave are requested at once: one memory round trip per
+// chunk).
 //   logits  S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (M = 16 keys, N = 16
 //           query-head columns of which n_q/n_kv <= 8 are used, K = 32
-//           channels).  K tiles of 32 rows are loaded fully coalesced (4 whole
-//           rows per 1 KB instruction), stored to LDS with padded rows and
-//           read back with ds_read_b128 in the A-operand layout.  The logits
+//           channels).  K tiles of 32 rows are loaded straight into the
+//           A-operand layout (each 1 KB instruction reads 64-byte pieces of
+//           16 rows) and used from registers.  The logits
 //           of the odd 16-key half of a tile are moved into the unused head
 //           columns 8..15 (DPP row rotate by 8), so 32 keys x 8 heads take 4
 //           registers per lane.
@@ -148,9 +149,9 @@ __device__ __forceinline__ bool resolve_chunk(const FusedArgs& a, int f, SeqItem
 
 // Attend kernel: work item = (layer, chunk, KV head), a workgroup of SPLIT_W
 // waves in which wave w owns keys [VT w, VT w + VT) of the chunk.  Each wave
-// requests its K and V tile (16 KB) before anything else, so a chunk costs
-// one memory round trip, and a one-layer call over 8k keys spreads its 16 MB
-// over 260 workgroups.  The waves agree on the chunk's max per head through
+// requests its query rows and its K and V tile (16 KB) before anything else,
+// so a chunk costs one memory round trip, and a one-layer call over 8k keys
+// spreads its 16 MB over 260 workgroups.  The waves agree on the chunk's max per head through
 // LDS, then sum their exp2 sums and partial outputs in wave order; the
 // partial results of (chunk, query head) go to the workspace for the
 // finishing kernels.  (Launch bounds: four workgroups per CU, 128 registers
