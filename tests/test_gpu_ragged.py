@@ -145,6 +145,15 @@ def test_ragged_decode_finishing_launches_agree():
     _run_decode_case(synth.DT_BF16, 128, 32, 4, [300, 17000], steps=1, seed=12)
 
 
+def test_ragged_decode_new_row_at_every_tile_row():
+    """Lengths 224..255 put the new K/V row of Eq. (1) in each of the 32 rows
+    of a wave's tile on the chunked path (2 layers x 4 KV heads): the wave
+    holding it takes it into its tile registers after its loads and writes
+    it to the cache from there; every sequence against the oracle and, bit
+    for bit, against its single-sequence call."""
+    _run_decode_case(synth.DT_BF16, 128, 32, 4, list(range(224, 256)), steps=1, seed=21)
+
+
 def test_ragged_decode_one_sequence_and_gamma_edges():
     _run_decode_case(synth.DT_BF16, 128, 32, 4, [2000], steps=1, gamma=1.0, seed=3)
     _run_decode_case(synth.DT_BF16, 128, 32, 4, [9, 300], steps=1, gamma=0.0, seed=4)
